@@ -1,0 +1,308 @@
+"""Plain CPU oracle of the FlashDiff region-sparse denoising step.
+
+TEST INFRASTRUCTURE ONLY.  Only tests/, __graft_entry__.smoke() and the
+cpu_baseline leg of bench.py may import this module.  The product path
+(paper_2607_12121_amd/) never imports it and shares no code with it.
+
+It is written to be read against the paper (FlashDiff, arXiv 2607.12121):
+numpy, one step of the method per function, float64 arithmetic except where the
+method itself fixes a narrower type:
+  * the region activity squares an fp32 difference of two fp32 latents;
+  * the latent update is fp32: x + fl32(h * v), two rounded fp32 operations,
+    because the latent is an fp32 tensor.
+Weights are the bf16 values the workload draws, used exactly (as float64).
+
+What each function follows:
+  region_score      Sec. 3.2 (Patch Gate): per-patch change signal.  Reading:
+                    the mean squared step-to-step latent delta over the region.
+  gate_select       Appendix "Setup and Notation": frozen change when skipped
+                    (eq. delta-i), normalised weight and threshold
+                    (eq. gate-weight), forced reactivation
+                    (eq. forced-reactivation); Alg. 1 PatchGate returns
+                    {i : w_i >= eps}.
+  active_rows       patch decomposition (Appendix "Setup and Notation"):
+                    tokens of active patches, ascending.
+  adaln, block_forward, final_layer, embed
+                    one adaLN DiT block on the active rows.  The paper serves
+                    DiT backbones (Sec. 2.1) without spelling out a block; the
+                    block is the standard adaLN DiT one.  K/V of skipped tokens
+                    come from the cache (Sec. 4 Backend; Prop. "Stale-KV
+                    Perturbation").
+  latent_update     eq. sf-update with the Euler step of eq. euler.
+
+Parity pins live in tests/test_oracle_pins.py; no function here is unpinned.
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+from typing import Dict, List, Optional
+
+import numpy as np
+
+LN_EPS = 1e-6
+FREEZE = 0          # skipped latent rows are left unchanged
+REUSE_DRIFT = 1     # skipped latent rows advance with their cached drift (eq. sf-update)
+
+
+@dataclass
+class Layout:
+    """Request-major token/region numbering, derived here from the region map alone."""
+
+    token_region: np.ndarray   # [N] global region of every token
+    req_tok_off: np.ndarray    # [B+1] token range of each request
+    n_regions: int
+
+    @property
+    def n_requests(self) -> int:
+        return len(self.req_tok_off) - 1
+
+    def token_request(self) -> np.ndarray:
+        n = int(self.req_tok_off[-1])
+        out = np.empty(n, dtype=np.int64)
+        for b in range(self.n_requests):
+            out[self.req_tok_off[b]:self.req_tok_off[b + 1]] = b
+        return out
+
+    def region_request(self) -> np.ndarray:
+        rr = np.full(self.n_regions, -1, dtype=np.int64)
+        treq = self.token_request()
+        for u, r in enumerate(self.token_region):
+            rr[r] = treq[u]
+        return rr
+
+    def region_tokens(self, r: int) -> np.ndarray:
+        return np.nonzero(self.token_region == r)[0]
+
+
+# ------------------------------------------------------------------ gate (a1, a2)
+
+def region_score(layout: Layout, x_cur: np.ndarray, x_prev: np.ndarray) -> np.ndarray:
+    """Activity of every region: mean over its tokens and channels of d^2, d = fl32(x_cur - x_prev).
+
+    d is one rounded fp32 subtraction; d^2 is exact in float64; the sum and the
+    division by (tokens * channels) are float64.
+    """
+    d = (x_cur.astype(np.float32) - x_prev.astype(np.float32)).astype(np.float64)
+    C = x_cur.shape[1]
+    out = np.zeros(layout.n_regions, dtype=np.float64)
+    for r in range(layout.n_regions):
+        toks = layout.region_tokens(r)
+        out[r] = np.sum(d[toks] ** 2) / (len(toks) * C)
+    return out
+
+
+def gate_select(layout: Layout, score: np.ndarray, s_tilde: np.ndarray, skip_run: np.ndarray,
+                prev_active: np.ndarray, eps: np.ndarray, eta: float, max_skip: int):
+    """One Patch Gate decision for every region.
+
+    1. Frozen change (eq. delta-i): a region executed at the previous step takes
+       its fresh score, a skipped one keeps its last value.
+    2. Per request b: D_b = sum_j (s~_j + eta)             (eq. gate-weight)
+    3. Skip iff w_i = (s~_i + eta) / D_b < eps_b, evaluated without the division
+       as (s~_i + eta) < eps_b * D_b; eps_b = +inf skips every region.
+    4. Forced reactivation (eq. forced-reactivation): a region that has been
+       skipped max_skip times in a row is active (max_skip = 0 disables it).
+    Returns (s_tilde', skip_run', active) with active as bool [R].
+    """
+    rreq = layout.region_request()
+    s_t = np.where(prev_active.astype(bool), score, s_tilde).astype(np.float64)
+    B = layout.n_requests
+    Db = np.zeros(B, dtype=np.float64)
+    for r in range(layout.n_regions):
+        Db[rreq[r]] += s_t[r] + eta
+    active = np.zeros(layout.n_regions, dtype=bool)
+    for r in range(layout.n_regions):
+        b = rreq[r]
+        forced = max_skip > 0 and skip_run[r] >= max_skip
+        if np.isposinf(eps[b]):
+            below = True
+        else:
+            below = bool((s_t[r] + eta) < eps[b] * Db[b])
+        active[r] = forced or not below
+    new_run = np.where(active, 0, skip_run.astype(np.int64) + 1).astype(np.int32)
+    return s_t, new_run, active
+
+
+def gate_weights(layout: Layout, s_tilde: np.ndarray, eta: float) -> np.ndarray:
+    """w_i = (s~_i + eta) / D_b (eq. gate-weight); used by property tests."""
+    rreq = layout.region_request()
+    Db = np.zeros(layout.n_requests)
+    for r in range(layout.n_regions):
+        Db[rreq[r]] += s_tilde[r] + eta
+    return (s_tilde + eta) / Db[rreq]
+
+
+def active_rows(layout: Layout, active: np.ndarray):
+    """Ascending global ids of tokens whose region is active, and per-request counts.
+
+    Returns idx int64 [M], cu_q int64 [B+1] (cu_q[b] = active tokens before request b).
+    """
+    tok_active = active[layout.token_region]
+    idx = np.nonzero(tok_active)[0]
+    B = layout.n_requests
+    cu = np.zeros(B + 1, dtype=np.int64)
+    for b in range(B):
+        lo, hi = layout.req_tok_off[b], layout.req_tok_off[b + 1]
+        cu[b + 1] = cu[b] + int(np.count_nonzero(tok_active[lo:hi]))
+    return idx, cu
+
+
+# ------------------------------------------------------------------ DiT pieces
+
+def silu(z: np.ndarray) -> np.ndarray:
+    return z / (1.0 + np.exp(-z))
+
+
+def gelu_tanh(z: np.ndarray) -> np.ndarray:
+    """GELU, tanh form: z/2 * (1 + tanh(sqrt(2/pi) * (z + 0.044715 z^3)))."""
+    return 0.5 * z * (1.0 + np.tanh(np.sqrt(2.0 / np.pi) * (z + 0.044715 * z ** 3)))
+
+
+def layer_norm(x: np.ndarray) -> np.ndarray:
+    """LayerNorm over the last axis, biased variance, eps 1e-6, no affine."""
+    mu = x.mean(axis=-1, keepdims=True)
+    var = ((x - mu) ** 2).mean(axis=-1, keepdims=True)
+    return (x - mu) / np.sqrt(var + LN_EPS)
+
+
+def modulate(x: np.ndarray, shift: np.ndarray, scale: np.ndarray) -> np.ndarray:
+    """adaLN modulation: x * (1 + scale) + shift."""
+    return x * (1.0 + scale) + shift
+
+
+def adaln(w_ada: np.ndarray, b_ada: np.ndarray, cond: np.ndarray, chunks: int) -> List[np.ndarray]:
+    """Modulation vectors per request: SiLU(c) W_ada^T + b_ada, split in `chunks` parts.
+
+    A block uses six (shift1, scale1, gate1, shift2, scale2, gate2); the final
+    layer two (shift, scale).  Each part is [B, D].
+    """
+    mod = silu(cond) @ w_ada.T + b_ada
+    return np.split(mod, chunks, axis=-1)
+
+
+def attention(q: np.ndarray, k: np.ndarray, v: np.ndarray) -> np.ndarray:
+    """softmax(q k^T / sqrt(dh)) v for one head; q [m, dh], k and v [n, dh]."""
+    s = q @ k.T / np.sqrt(q.shape[-1])
+    s = s - s.max(axis=-1, keepdims=True)
+    p = np.exp(s)
+    p = p / p.sum(axis=-1, keepdims=True)
+    return p @ v
+
+
+def embed(xa: np.ndarray, idx: np.ndarray, w_e: np.ndarray, b_e: np.ndarray, pos: np.ndarray) -> np.ndarray:
+    """Token embedding of the gathered latent rows: xa W_e^T + b_e + pos[token]."""
+    return xa @ w_e.T + b_e + pos[idx]
+
+
+def block_forward(h: np.ndarray, idx: np.ndarray, row_req: np.ndarray, layout: Layout,
+                  blk: Dict[str, np.ndarray], cond: np.ndarray, k_cache: np.ndarray,
+                  v_cache: np.ndarray, n_heads: int) -> np.ndarray:
+    """One adaLN DiT block on the active rows h [M, D] (token ids idx, requests row_req).
+
+    k_cache / v_cache [N, D] are updated in place: the rows of the active tokens
+    are overwritten with this step's keys and values before attention; rows of
+    skipped tokens keep what an earlier step wrote (stale K/V).  Each active
+    query attends to every token of its own request.
+    """
+    M, D = h.shape
+    dh = D // n_heads
+    shift1, scale1, gate1, shift2, scale2, gate2 = adaln(blk["w_ada"], blk["b_ada"], cond, 6)
+    a = modulate(layer_norm(h), shift1[row_req], scale1[row_req])
+    qkv = a @ blk["w_qkv"].T + blk["b_qkv"]
+    q, k, v = qkv[:, :D], qkv[:, D:2 * D], qkv[:, 2 * D:]
+    k_cache[idx] = k
+    v_cache[idx] = v
+    o = np.zeros((M, D))
+    for b in range(layout.n_requests):
+        rows = np.nonzero(row_req == b)[0]
+        if len(rows) == 0:
+            continue
+        lo, hi = layout.req_tok_off[b], layout.req_tok_off[b + 1]
+        for hd in range(n_heads):
+            c = slice(hd * dh, (hd + 1) * dh)
+            o[rows, c] = attention(q[rows, c], k_cache[lo:hi, c], v_cache[lo:hi, c])
+    h = h + gate1[row_req] * (o @ blk["w_o"].T + blk["b_o"])
+    a = modulate(layer_norm(h), shift2[row_req], scale2[row_req])
+    mlp = gelu_tanh(a @ blk["w_1"].T + blk["b_1"]) @ blk["w_2"].T + blk["b_2"]
+    return h + gate2[row_req] * mlp
+
+
+def final_layer(h: np.ndarray, row_req: np.ndarray, w_adaf: np.ndarray, b_adaf: np.ndarray,
+                w_out: np.ndarray, b_out: np.ndarray, cond: np.ndarray) -> np.ndarray:
+    """Velocity of the active rows: modulate(LN(h), shift, scale) W_out^T + b_out."""
+    shift, scale = adaln(w_adaf, b_adaf, cond, 2)
+    return modulate(layer_norm(h), shift[row_req], scale[row_req]) @ w_out.T + b_out
+
+
+# ------------------------------------------------------------------ update (a14)
+
+def latent_update(x: np.ndarray, v: np.ndarray, idx: np.ndarray, layout: Layout, dt: np.ndarray,
+                  vcache: np.ndarray, active: np.ndarray, skip_mode: int):
+    """Euler update of eq. sf-update on the fp32 latent; returns (x', vcache').
+
+    Active tokens: x + fl32(h * f) with f = fl32(v), and the cached drift of the
+    token becomes f.  Skipped tokens: unchanged (FREEZE) or x + fl32(h * c) with
+    c the cached drift (REUSE_DRIFT, the paper's rule).  Every operation is one
+    rounded fp32 operation (numpy does not contract them).
+    """
+    x = np.array(x, dtype=np.float32, copy=True)
+    vc = np.array(vcache, dtype=np.float32, copy=True)
+    treq = layout.token_request()
+    dt = np.asarray(dt, dtype=np.float32)
+    tok_active = active[layout.token_region]
+    if skip_mode == REUSE_DRIFT:
+        sk = np.nonzero(~tok_active)[0]
+        step = dt[treq[sk]][:, None] * vc[sk]
+        x[sk] = x[sk] + step
+    f = np.asarray(v, dtype=np.float32)
+    step = dt[treq[idx]][:, None] * f
+    x[idx] = x[idx] + step
+    vc[idx] = f
+    return x, vc
+
+
+# ------------------------------------------------------------------ whole step
+
+@dataclass
+class GateState:
+    s_tilde: np.ndarray      # fp64 [R] frozen change
+    skip_run: np.ndarray     # int32 [R] consecutive skips
+    active: np.ndarray       # bool [R] previous decision
+
+    @staticmethod
+    def fresh(R: int) -> "GateState":
+        return GateState(np.zeros(R), np.zeros(R, np.int32), np.ones(R, bool))
+
+
+def params_block(params: Dict[str, np.ndarray], l: int) -> Dict[str, np.ndarray]:
+    return {k: params[k][l] for k in ("w_qkv", "b_qkv", "w_o", "b_o", "w_1", "b_1",
+                                      "w_2", "b_2", "w_ada", "b_ada")}
+
+
+def sparse_step(layout: Layout, params: Dict[str, np.ndarray], n_heads: int, cond: np.ndarray,
+                x_cur: np.ndarray, x_prev: np.ndarray, gate: GateState, eps: np.ndarray,
+                eta: float, max_skip: int, k_cache: List[np.ndarray], v_cache: List[np.ndarray],
+                vcache: np.ndarray, dt: np.ndarray, skip_mode: int = FREEZE, n_layers: Optional[int] = None):
+    """One region-sparse denoising step (score, gate, gather, blocks, update).
+
+    params holds float64 arrays: per-block w_*/b_* stacked on axis 0, plus
+    w_e, b_e, pos, w_adaf, b_adaf, w_out, b_out.  k_cache/v_cache are per-block
+    [N, D] float64 arrays updated in place.  Returns a dict with the new latent,
+    drift cache and gate state, the active mask, idx, cu_q, h and v.
+    """
+    score = region_score(layout, x_cur, x_prev)
+    s_t, run, active = gate_select(layout, score, gate.s_tilde, gate.skip_run, gate.active,
+                                   eps, eta, max_skip)
+    idx, cu = active_rows(layout, active)
+    row_req = layout.token_request()[idx]
+    xa = x_cur[idx].astype(np.float64)
+    h = embed(xa, idx, params["w_e"], params["b_e"], params["pos"])
+    L = params["w_qkv"].shape[0] if n_layers is None else n_layers
+    for l in range(L):
+        h = block_forward(h, idx, row_req, layout, params_block(params, l), cond,
+                          k_cache[l], v_cache[l], n_heads)
+    v = final_layer(h, row_req, params["w_adaf"], params["b_adaf"], params["w_out"],
+                    params["b_out"], cond)
+    x_new, vc_new = latent_update(x_cur, v, idx, layout, dt, vcache, active, skip_mode)
+    return dict(score=score, active=active, idx=idx, cu_q=cu, h=h, v=v, x=x_new, vcache=vc_new,
+                gate=GateState(s_t, run, active))
