@@ -74,7 +74,7 @@ class Layout:
         return np.nonzero(self.token_region == r)[0]
 
 
-# ------------------------------------------------------------------ gate (a1, a2)
+# ------------------------------------------------------------------ gate
 
 def region_score(layout: Layout, x_cur: np.ndarray, x_prev: np.ndarray) -> np.ndarray:
     """Activity of every region: mean over its tokens and channels of d^2, d = fl32(x_cur - x_prev).
@@ -196,13 +196,15 @@ def embed(xa: np.ndarray, idx: np.ndarray, w_e: np.ndarray, b_e: np.ndarray, pos
 
 def block_forward(h: np.ndarray, idx: np.ndarray, row_req: np.ndarray, layout: Layout,
                   blk: Dict[str, np.ndarray], cond: np.ndarray, k_cache: np.ndarray,
-                  v_cache: np.ndarray, n_heads: int) -> np.ndarray:
+                  v_cache: np.ndarray, n_heads: int, out_rows: Optional[np.ndarray] = None) -> np.ndarray:
     """One adaLN DiT block on the active rows h [M, D] (token ids idx, requests row_req).
 
     k_cache / v_cache [N, D] are updated in place: the rows of the active tokens
     are overwritten with this step's keys and values before attention; rows of
     skipped tokens keep what an earlier step wrote (stale K/V).  Each active
-    query attends to every token of its own request.
+    query attends to every token of its own request.  Once the caches are
+    written the rows are independent, so `out_rows` (indices into the M rows)
+    restricts the rest of the block to those rows and returns only them.
     """
     M, D = h.shape
     dh = D // n_heads
@@ -212,6 +214,9 @@ def block_forward(h: np.ndarray, idx: np.ndarray, row_req: np.ndarray, layout: L
     q, k, v = qkv[:, :D], qkv[:, D:2 * D], qkv[:, 2 * D:]
     k_cache[idx] = k
     v_cache[idx] = v
+    if out_rows is not None:
+        h, q, row_req = h[out_rows], q[out_rows], row_req[out_rows]
+        M = len(out_rows)
     o = np.zeros((M, D))
     for b in range(layout.n_requests):
         rows = np.nonzero(row_req == b)[0]
@@ -234,7 +239,7 @@ def final_layer(h: np.ndarray, row_req: np.ndarray, w_adaf: np.ndarray, b_adaf: 
     return modulate(layer_norm(h), shift[row_req], scale[row_req]) @ w_out.T + b_out
 
 
-# ------------------------------------------------------------------ update (a14)
+# ------------------------------------------------------------------ update
 
 def latent_update(x: np.ndarray, v: np.ndarray, idx: np.ndarray, layout: Layout, dt: np.ndarray,
                   vcache: np.ndarray, active: np.ndarray, skip_mode: int):
@@ -282,13 +287,18 @@ def params_block(params: Dict[str, np.ndarray], l: int) -> Dict[str, np.ndarray]
 def sparse_step(layout: Layout, params: Dict[str, np.ndarray], n_heads: int, cond: np.ndarray,
                 x_cur: np.ndarray, x_prev: np.ndarray, gate: GateState, eps: np.ndarray,
                 eta: float, max_skip: int, k_cache: List[np.ndarray], v_cache: List[np.ndarray],
-                vcache: np.ndarray, dt: np.ndarray, skip_mode: int = FREEZE, n_layers: Optional[int] = None):
+                vcache: np.ndarray, dt: np.ndarray, skip_mode: int = FREEZE, n_layers: Optional[int] = None,
+                sample_rows: Optional[np.ndarray] = None):
     """One region-sparse denoising step (score, gate, gather, blocks, update).
 
     params holds float64 arrays: per-block w_*/b_* stacked on axis 0, plus
     w_e, b_e, pos, w_adaf, b_adaf, w_out, b_out.  k_cache/v_cache are per-block
     [N, D] float64 arrays updated in place.  Returns a dict with the new latent,
     drift cache and gate state, the active mask, idx, cu_q, h and v.
+
+    sample_rows (indices into the M active rows) restricts the last block, the
+    final layer and the active-row update to those rows: h and v then hold only
+    them, and x is updated only on their tokens (and on skipped tokens).
     """
     score = region_score(layout, x_cur, x_prev)
     s_t, run, active = gate_select(layout, score, gate.s_tilde, gate.skip_run, gate.active,
@@ -298,11 +308,15 @@ def sparse_step(layout: Layout, params: Dict[str, np.ndarray], n_heads: int, con
     xa = x_cur[idx].astype(np.float64)
     h = embed(xa, idx, params["w_e"], params["b_e"], params["pos"])
     L = params["w_qkv"].shape[0] if n_layers is None else n_layers
+    rows = np.arange(len(idx)) if sample_rows is None else np.asarray(sample_rows)
     for l in range(L):
+        last = sample_rows is not None and l == L - 1
         h = block_forward(h, idx, row_req, layout, params_block(params, l), cond,
-                          k_cache[l], v_cache[l], n_heads)
-    v = final_layer(h, row_req, params["w_adaf"], params["b_adaf"], params["w_out"],
+                          k_cache[l], v_cache[l], n_heads, out_rows=rows if last else None)
+    if sample_rows is not None and L == 0:
+        h = h[rows]
+    v = final_layer(h, row_req[rows], params["w_adaf"], params["b_adaf"], params["w_out"],
                     params["b_out"], cond)
-    x_new, vc_new = latent_update(x_cur, v, idx, layout, dt, vcache, active, skip_mode)
+    x_new, vc_new = latent_update(x_cur, v, idx[rows], layout, dt, vcache, active, skip_mode)
     return dict(score=score, active=active, idx=idx, cu_q=cu, h=h, v=v, x=x_new, vcache=vc_new,
-                gate=GateState(s_t, run, active))
+                gate=GateState(s_t, run, active), rows=rows)

@@ -1,0 +1,113 @@
+// Internal helpers shared by the HIP kernels of the region-sparse step (gfx950).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "flashdiff.h"
+
+#define FD_DEVICE __device__ __forceinline__
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+namespace fd {
+
+constexpr int kWave = 64;
+
+// fp32 -> bf16 bits, round to nearest even (hardware conversion on gfx950).
+FD_DEVICE uint16_t f2bf(float x) { return __builtin_bit_cast(uint16_t, static_cast<__bf16>(x)); }
+FD_DEVICE float bf2f(uint16_t b) { return __uint_as_float(static_cast<uint32_t>(b) << 16); }
+FD_DEVICE uint32_t pack_bf2(float lo, float hi) {
+  return static_cast<uint32_t>(f2bf(lo)) | (static_cast<uint32_t>(f2bf(hi)) << 16);
+}
+
+FD_DEVICE float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+FD_DEVICE double wave_sum(double v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+FD_DEVICE int wave_sum(int v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+
+// Request of active row i: the b with cu_q[b] <= i < cu_q[b+1] (B is small; uniform loads).
+FD_DEVICE int row_request(const int32_t* __restrict__ cu_q, int B, int i) {
+  int b = 0;
+  while (b + 1 < B && cu_q[b + 1] <= i) ++b;
+  return b;
+}
+
+FD_DEVICE float gelu_tanh(float z) {
+  const float k0 = 0.7978845608028654f;  // sqrt(2/pi)
+  const float u = k0 * (z + 0.044715f * z * z * z);
+  return 0.5f * z * (1.0f + tanhf(u));
+}
+
+}  // namespace fd
+
+// ------------------------------------------------------------------ host side
+
+namespace fdh {
+
+// Thread-local error message (set on failure, read by fd_last_error).
+void set_error(const char* fmt, ...);
+fd_status hip_fail(hipError_t e, const char* what);
+
+// Timer hooks around a launch (no-ops unless the timer is armed for `kernel`).
+void timer_begin(int kernel, hipStream_t s);
+void timer_end(int kernel, hipStream_t s);
+
+int num_cus();
+
+// Launchers (defined in the kernel files; arguments already validated).
+hipError_t launch_region_score(const fd_plan* p, int C, const float* xc, const float* xp, double* score,
+                               double* partial, int nchunk, int rows_per_chunk, hipStream_t s);
+hipError_t launch_select(const fd_plan* p, const double* score, const double* eps, fd_gate g,
+                         double* s_tilde, int32_t* skip_run, const uint8_t* prev_active, uint8_t* active,
+                         int32_t* idx, int32_t* cu_q, int32_t* m, hipStream_t s);
+hipError_t launch_gather(const fd_plan* p, int C, const float* x, const int32_t* idx, const int32_t* m,
+                         uint16_t* xa, hipStream_t s);
+hipError_t launch_scatter_update(const fd_plan* p, int C, float* x, const float* v, const int32_t* idx,
+                                 const int32_t* m, const float* dt, float* vcache, const uint8_t* active,
+                                 int skip_mode, hipStream_t s);
+hipError_t launch_adaln(const uint16_t* w, const float* b, const float* cond, int B, int D, int n_out,
+                        float* mod, hipStream_t s);
+hipError_t launch_ln_modulate(const float* h, const int32_t* cu_q, int B, const int32_t* m, int n_max, int D,
+                              const float* mod, int mod_stride, int shift_off, int scale_off, uint16_t* a,
+                              hipStream_t s);
+
+// GEMM epilogue kinds.
+enum GemmKind { GEMM_QKV = 0, GEMM_RESID = 1, GEMM_GELU = 2, GEMM_EMBED = 3, GEMM_OUT = 4 };
+
+struct GemmArgs {
+  const uint16_t* act;   // [M][K] bf16 activations
+  const uint16_t* wt;    // [N][K] bf16 weights
+  const float* bias;     // [N]
+  int n_max;             // row capacity (upper bound of M)
+  const int32_t* m;      // device active row count
+  int N, K;
+  // epilogue operands
+  const int32_t* idx;    // token of each row (QKV cache scatter, EMBED position)
+  const int32_t* cu_q; int n_req;
+  uint16_t* out_bf16;    // QKV: q [M][D]; GELU: g [M][N]
+  uint16_t* k_cache; uint16_t* v_cache; int D;  // QKV
+  float* out_f32;        // RESID: h [M][N] (+=); EMBED: h [M][N]; OUT: v [M][N]
+  const float* gate; int gate_stride;          // RESID: gate row per request
+  const float* pos;      // EMBED: [N_tok][N]
+};
+hipError_t launch_gemm(GemmKind kind, const GemmArgs& a, hipStream_t s);
+
+hipError_t launch_attention(const uint16_t* q, const uint16_t* kc, const uint16_t* vc, uint16_t* o, int D, int H,
+                            int dh, const int32_t* cu_q, const int32_t* req_tok_off, int B, int n_max,
+                            const int32_t* m, hipStream_t s);
+
+}  // namespace fdh

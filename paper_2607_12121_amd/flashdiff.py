@@ -1,0 +1,318 @@
+"""Python binding of libflashdiff.so (the region-sparse DiT step's C ABI).
+
+Argument marshalling only: every function below passes device pointers, sizes
+and torch's current HIP stream to the C entry point of the same name; all
+computation runs in the library's HIP kernels.  torch provides device memory
+and streams.  If the library is missing this module raises on import of the
+library (there is no fallback path).
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass
+from typing import Dict, Optional, Sequence
+
+import numpy as np
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libflashdiff.so")
+
+FD_SKIP_FREEZE = 0
+FD_SKIP_REUSE_DRIFT = 1
+
+KERNELS = {"score": 1, "select": 2, "gather": 3, "embed": 4, "adaln": 5, "ln": 6, "gemm_qkv": 7,
+           "attn": 8, "gemm_o": 9, "gemm_mlp1": 10, "gemm_mlp2": 11, "final": 12, "scatter": 13}
+
+_p = ctypes.c_void_p
+_i32 = ctypes.c_int32
+
+
+class FdPlan(ctypes.Structure):
+    _fields_ = [("n_tokens", _i32), ("n_regions", _i32), ("n_requests", _i32),
+                ("max_region_tokens", _i32), ("max_request_tokens", _i32),
+                ("region_ptr", _p), ("region_tokens", _p), ("region_req", _p),
+                ("token_region", _p), ("req_tok_off", _p), ("req_reg_off", _p)]
+
+
+class FdDims(ctypes.Structure):
+    _fields_ = [("C", _i32), ("D", _i32), ("H", _i32), ("dh", _i32), ("F", _i32)]
+
+
+class FdBlockWeights(ctypes.Structure):
+    _fields_ = [(n, _p) for n in ("w_qkv", "b_qkv", "w_o", "b_o", "w_1", "b_1", "w_2", "b_2",
+                                  "w_ada", "b_ada")]
+
+
+class FdFinalWeights(ctypes.Structure):
+    _fields_ = [(n, _p) for n in ("w_ada", "b_ada", "w_out", "b_out")]
+
+
+class FdGate(ctypes.Structure):
+    _fields_ = [("eta", ctypes.c_double), ("max_skip", _i32)]
+
+
+class FlashDiffError(RuntimeError):
+    pass
+
+
+_lib: Optional[ctypes.CDLL] = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libflashdiff.so (built by paper_2607_12121_amd.build); raise if it is missing."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise FlashDiffError(f"{LIB_PATH} is missing: build it with `python -m paper_2607_12121_amd.build`")
+    L = ctypes.CDLL(LIB_PATH)
+    P = ctypes.POINTER
+    sig = {
+        "fd_last_error": ([], ctypes.c_char_p),
+        "fd_version": ([], ctypes.c_char_p),
+        "fd_plan_build": ([_i32, _i32, _i32, _p, _p, _p, _p, _p, _p, _p, _p], _i32),
+        "fd_region_score_ws_size": ([P(FdPlan), _i32], ctypes.c_size_t),
+        "fd_region_score": ([P(FdPlan), _i32, _p, _p, _p, _p, ctypes.c_size_t, _p], _i32),
+        "fd_select": ([P(FdPlan), _p, _p, FdGate, _p, _p, _p, _p, _p, _p, _p, _p], _i32),
+        "fd_gather": ([P(FdPlan), _i32, _p, _p, _p, _p, _p], _i32),
+        "fd_embed": ([P(FdPlan), P(FdDims), _p, _p, _p, _p, _p, _p, _p, _p], _i32),
+        "fd_block_ws_size": ([P(FdPlan), P(FdDims)], ctypes.c_size_t),
+        "fd_block_forward": ([P(FdPlan), P(FdDims), P(FdBlockWeights), _p, _p, _p, _p, _p, _p, _p, _p,
+                              ctypes.c_size_t, _p], _i32),
+        "fd_final": ([P(FdPlan), P(FdDims), P(FdFinalWeights), _p, _p, _p, _p, _p, _p, ctypes.c_size_t, _p],
+                     _i32),
+        "fd_scatter_update": ([P(FdPlan), _i32, _p, _p, _p, _p, _p, _p, _p, _i32, _p], _i32),
+        "fd_timer_arm": ([_i32, _i32], _i32),
+        "fd_timer_read": ([_p, _i32], _i32),
+        "fd_timer_disarm": ([], None),
+    }
+    for name, (args, res) in sig.items():
+        f = getattr(L, name)
+        f.argtypes = args
+        f.restype = res
+    _lib = L
+    return L
+
+
+def exported_symbols() -> Sequence[str]:
+    return ("fd_last_error", "fd_version", "fd_plan_build", "fd_region_score_ws_size", "fd_region_score",
+            "fd_select", "fd_gather", "fd_embed", "fd_block_ws_size", "fd_block_forward", "fd_final",
+            "fd_scatter_update", "fd_timer_arm", "fd_timer_read", "fd_timer_disarm")
+
+
+def _check(name: str, status: int) -> None:
+    if status != 0:
+        msg = lib().fd_last_error().decode(errors="replace")
+        raise FlashDiffError(f"{name} failed with status {status}: {msg}")
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise FlashDiffError("tensor arguments must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream: Optional[torch.cuda.Stream] = None) -> int:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+def version() -> str:
+    return lib().fd_version().decode()
+
+
+# ------------------------------------------------------------------ plan
+
+@dataclass
+class Plan:
+    """Region plan uploaded to the device, with its C descriptor."""
+
+    c: FdPlan
+    tensors: Dict[str, torch.Tensor]
+    host: Dict[str, np.ndarray]
+
+    @property
+    def n_tokens(self) -> int:
+        return self.c.n_tokens
+
+    @property
+    def n_regions(self) -> int:
+        return self.c.n_regions
+
+    @property
+    def n_requests(self) -> int:
+        return self.c.n_requests
+
+
+def fd_plan_build(token_region: np.ndarray, req_tok_off: np.ndarray, n_regions: int) -> Dict[str, np.ndarray]:
+    """Host CSR plan (calls the C builder)."""
+    tr = np.ascontiguousarray(token_region, dtype=np.int32)
+    to = np.ascontiguousarray(req_tok_off, dtype=np.int32)
+    N, B = len(tr), len(to) - 1
+    out = {"region_ptr": np.zeros(n_regions + 1, np.int32), "region_tokens": np.zeros(N, np.int32),
+           "region_req": np.zeros(n_regions, np.int32), "req_reg_off": np.zeros(B + 1, np.int32)}
+    mx_r, mx_b = _i32(0), _i32(0)
+    st = lib().fd_plan_build(N, n_regions, B, tr.ctypes.data, to.ctypes.data, out["region_ptr"].ctypes.data,
+                             out["region_tokens"].ctypes.data, out["region_req"].ctypes.data,
+                             out["req_reg_off"].ctypes.data, ctypes.addressof(mx_r), ctypes.addressof(mx_b))
+    _check("fd_plan_build", st)
+    out["token_region"] = tr
+    out["req_tok_off"] = to
+    out["max_region_tokens"] = np.int32(mx_r.value)
+    out["max_request_tokens"] = np.int32(mx_b.value)
+    return out
+
+
+def make_plan(token_region: np.ndarray, req_tok_off: np.ndarray, n_regions: int, device="cuda") -> Plan:
+    host = fd_plan_build(token_region, req_tok_off, n_regions)
+    keys = ("region_ptr", "region_tokens", "region_req", "token_region", "req_tok_off", "req_reg_off")
+    t = {k: torch.from_numpy(host[k]).to(device) for k in keys}
+    c = FdPlan(len(host["token_region"]), n_regions, len(host["req_tok_off"]) - 1,
+               int(host["max_region_tokens"]), int(host["max_request_tokens"]),
+               *[t[k].data_ptr() for k in keys])
+    return Plan(c, t, host)
+
+
+def dims(C: int, D: int, H: int, dh: int, F: int) -> FdDims:
+    return FdDims(C, D, H, dh, F)
+
+
+# ------------------------------------------------------------------ entry points
+
+def fd_region_score_ws_size(plan: Plan, C: int) -> int:
+    return int(lib().fd_region_score_ws_size(ctypes.byref(plan.c), C))
+
+
+def fd_region_score(plan: Plan, C: int, x_cur, x_prev, score, ws, stream=None) -> None:
+    _check("fd_region_score", lib().fd_region_score(ctypes.byref(plan.c), C, _ptr(x_cur), _ptr(x_prev),
+                                                    _ptr(score), _ptr(ws), ws.numel() * ws.element_size(),
+                                                    _stream(stream)))
+
+
+def fd_select(plan: Plan, score, eps, eta: float, max_skip: int, s_tilde, skip_run, prev_active, active,
+              idx, cu_q, m, stream=None) -> None:
+    _check("fd_select", lib().fd_select(ctypes.byref(plan.c), _ptr(score), _ptr(eps), FdGate(eta, max_skip),
+                                        _ptr(s_tilde), _ptr(skip_run), _ptr(prev_active), _ptr(active),
+                                        _ptr(idx), _ptr(cu_q), _ptr(m), _stream(stream)))
+
+
+def fd_gather(plan: Plan, C: int, x_cur, idx, m, xa, stream=None) -> None:
+    _check("fd_gather", lib().fd_gather(ctypes.byref(plan.c), C, _ptr(x_cur), _ptr(idx), _ptr(m), _ptr(xa),
+                                        _stream(stream)))
+
+
+def fd_embed(plan: Plan, d: FdDims, xa, w_e, b_e, pos, idx, m, h, stream=None) -> None:
+    _check("fd_embed", lib().fd_embed(ctypes.byref(plan.c), ctypes.byref(d), _ptr(xa), _ptr(w_e), _ptr(b_e),
+                                      _ptr(pos), _ptr(idx), _ptr(m), _ptr(h), _stream(stream)))
+
+
+def fd_block_ws_size(plan: Plan, d: FdDims) -> int:
+    return int(lib().fd_block_ws_size(ctypes.byref(plan.c), ctypes.byref(d)))
+
+
+def block_weights(params: Dict[str, torch.Tensor], l: int) -> FdBlockWeights:
+    names = ("w_qkv", "b_qkv", "w_o", "b_o", "w_1", "b_1", "w_2", "b_2", "w_ada", "b_ada")
+    return FdBlockWeights(*[_ptr(params[n][l]) for n in names])
+
+
+def final_weights(params: Dict[str, torch.Tensor]) -> FdFinalWeights:
+    return FdFinalWeights(_ptr(params["w_adaf"]), _ptr(params["b_adaf"]), _ptr(params["w_out"]),
+                          _ptr(params["b_out"]))
+
+
+def fd_block_forward(plan: Plan, d: FdDims, w: FdBlockWeights, cond, h, idx, cu_q, m, k_cache, v_cache, ws,
+                     stream=None) -> None:
+    _check("fd_block_forward", lib().fd_block_forward(
+        ctypes.byref(plan.c), ctypes.byref(d), ctypes.byref(w), _ptr(cond), _ptr(h), _ptr(idx), _ptr(cu_q),
+        _ptr(m), _ptr(k_cache), _ptr(v_cache), _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def fd_final(plan: Plan, d: FdDims, w: FdFinalWeights, cond, h, cu_q, m, v, ws, stream=None) -> None:
+    _check("fd_final", lib().fd_final(ctypes.byref(plan.c), ctypes.byref(d), ctypes.byref(w), _ptr(cond), _ptr(h),
+                                      _ptr(cu_q), _ptr(m), _ptr(v), _ptr(ws), ws.numel() * ws.element_size(),
+                                      _stream(stream)))
+
+
+def fd_scatter_update(plan: Plan, C: int, x, v, idx, m, dt, vcache, active, skip_mode: int, stream=None) -> None:
+    _check("fd_scatter_update", lib().fd_scatter_update(ctypes.byref(plan.c), C, _ptr(x), _ptr(v), _ptr(idx),
+                                                        _ptr(m), _ptr(dt), _ptr(vcache), _ptr(active),
+                                                        skip_mode, _stream(stream)))
+
+
+def fd_timer_arm(kernel: str, capacity: int) -> None:
+    _check("fd_timer_arm", lib().fd_timer_arm(KERNELS[kernel], capacity))
+
+
+def fd_timer_read(capacity: int) -> np.ndarray:
+    out = np.zeros(capacity, np.float32)
+    n = lib().fd_timer_read(out.ctypes.data, capacity)
+    return out[:n]
+
+
+def fd_timer_disarm() -> None:
+    lib().fd_timer_disarm()
+
+
+# ------------------------------------------------------------------ step state
+
+class SparseStep:
+    """Device buffers of one batch and the call sequence of one region-sparse step.
+
+    Holds the plan, model parameters (device tensors from workloads.make_params),
+    per-block K/V caches, the gate state and the row workspaces; `step()` issues
+    fd_region_score, fd_select, fd_gather, fd_embed, L x fd_block_forward,
+    fd_final and fd_scatter_update on the current stream.
+    """
+
+    def __init__(self, plan: Plan, d: FdDims, params: Dict[str, torch.Tensor], n_layers: int,
+                 k_cache: Optional[torch.Tensor] = None, v_cache: Optional[torch.Tensor] = None,
+                 device: str = "cuda"):
+        self.plan, self.d, self.params, self.L = plan, d, params, n_layers
+        N, R, B, C, D = plan.n_tokens, plan.n_regions, plan.n_requests, d.C, d.D
+        dev = torch.device(device)
+        self.k_cache = k_cache if k_cache is not None else torch.zeros((n_layers, N, D), dtype=torch.bfloat16,
+                                                                        device=dev)
+        self.v_cache = v_cache if v_cache is not None else torch.zeros((n_layers, N, D), dtype=torch.bfloat16,
+                                                                        device=dev)
+        self.score = torch.zeros(R, dtype=torch.float64, device=dev)
+        self.s_tilde = torch.zeros(R, dtype=torch.float64, device=dev)
+        self.skip_run = torch.zeros(R, dtype=torch.int32, device=dev)
+        self.active = torch.ones(R, dtype=torch.uint8, device=dev)
+        self.idx = torch.zeros(N, dtype=torch.int32, device=dev)
+        self.cu_q = torch.zeros(B + 1, dtype=torch.int32, device=dev)
+        self.m = torch.zeros(1, dtype=torch.int32, device=dev)
+        self.xa = torch.zeros((N, C), dtype=torch.bfloat16, device=dev)
+        self.h = torch.zeros((N, D), dtype=torch.float32, device=dev)
+        self.v = torch.zeros((N, C), dtype=torch.float32, device=dev)
+        self.vcache = torch.zeros((N, C), dtype=torch.float32, device=dev)
+        self.ws_score = torch.empty(max(fd_region_score_ws_size(plan, C), 256), dtype=torch.uint8, device=dev)
+        self.ws_block = torch.empty(fd_block_ws_size(plan, d), dtype=torch.uint8, device=dev)
+        self.block_w = [block_weights(params, l) for l in range(n_layers)]
+        self.final_w = final_weights(params)
+
+    def reset_gate(self) -> None:
+        self.s_tilde.zero_()
+        self.skip_run.zero_()
+        self.active.fill_(1)
+
+    def step(self, x: torch.Tensor, x_prev: torch.Tensor, eps: torch.Tensor, dt: torch.Tensor,
+             cond: torch.Tensor, eta: float = 0.0, max_skip: int = 0, skip_mode: int = FD_SKIP_FREEZE,
+             stateless: bool = False, stream=None) -> None:
+        """One step on the latent x (updated in place); eps fp64 [B], dt fp32 [B], cond fp32 [B, D]."""
+        p, d, C = self.plan, self.d, self.d.C
+        if stateless:
+            self.active.fill_(1)
+        fd_region_score(p, C, x, x_prev, self.score, self.ws_score, stream)
+        fd_select(p, self.score, eps, eta, max_skip, self.s_tilde, self.skip_run, self.active, self.active,
+                  self.idx, self.cu_q, self.m, stream)
+        fd_gather(p, C, x, self.idx, self.m, self.xa, stream)
+        fd_embed(p, d, self.xa, self.params["w_e"], self.params["b_e"], self.params["pos"], self.idx, self.m,
+                 self.h, stream)
+        for l in range(self.L):
+            fd_block_forward(p, d, self.block_w[l], cond, self.h, self.idx, self.cu_q, self.m, self.k_cache[l],
+                             self.v_cache[l], self.ws_block, stream)
+        fd_final(p, d, self.final_w, cond, self.h, self.cu_q, self.m, self.v, self.ws_block, stream)
+        fd_scatter_update(p, C, x, self.v, self.idx, self.m, dt, self.vcache, self.active, skip_mode, stream)

@@ -1,0 +1,110 @@
+"""CPU tests of the C ABI: the library loads, exports every declared entry point,
+builds region plans, and rejects bad arguments before touching the GPU."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2607_12121_amd import flashdiff as fdl
+from paper_2607_12121_amd import workloads as wl
+
+HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "flashdiff.h")
+
+
+def _declared():
+    src = open(HEADER).read()
+    src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+    return sorted(set(re.findall(r"\b(fd_[a-z_]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = fdl.lib()
+    names = _declared()
+    assert len(names) >= 15
+    for n in names:
+        assert hasattr(lib, n), n
+    assert set(fdl.exported_symbols()) == set(names)
+    assert "gfx950" in fdl.version()
+
+
+@pytest.mark.parametrize("name", list(wl.WORKLOADS))
+def test_plan_build_matches_region_map(name):
+    w = wl.WORKLOADS[name]
+    rm = wl.region_map(w)
+    host = fdl.fd_plan_build(rm.token_region, rm.req_tok_off, rm.n_regions)
+    np.testing.assert_array_equal(host["req_reg_off"], rm.req_reg_off)
+    np.testing.assert_array_equal(host["region_req"], rm.region_req)
+    counts = np.bincount(rm.token_region, minlength=rm.n_regions)
+    np.testing.assert_array_equal(np.diff(host["region_ptr"]), counts)
+    for r in range(0, rm.n_regions, max(1, rm.n_regions // 17)):
+        toks = host["region_tokens"][host["region_ptr"][r]:host["region_ptr"][r + 1]]
+        np.testing.assert_array_equal(toks, np.nonzero(rm.token_region == r)[0])
+    assert host["max_region_tokens"] == counts.max()
+    assert host["max_request_tokens"] == np.diff(rm.req_tok_off).max()
+
+
+@pytest.mark.parametrize("token_region,req_tok_off,R,why", [
+    ([0, 1, 2], [0, 3], 4, "empty region"),
+    ([0, 1, 5], [0, 3], 3, "region id out of range"),
+    ([0, 1, 0, 1], [0, 2, 4], 2, "region spanning two requests"),
+    ([1, 1, 0, 0], [0, 2, 4], 2, "regions not request-major"),
+    ([0, 0], [0, 1, 1, 2], 1, "empty request"),
+    ([0, 0], [0, 3], 1, "request offsets do not end at N"),
+])
+def test_plan_build_rejects_bad_maps(token_region, req_tok_off, R, why):
+    with pytest.raises(fdl.FlashDiffError):
+        fdl.fd_plan_build(np.array(token_region), np.array(req_tok_off), R)
+
+
+def _fake_plan():
+    # host-only descriptor with non-null dummy addresses: validation never dereferences them
+    return fdl.FdPlan(16, 4, 1, 4, 16, *([0x1000] * 6))
+
+
+def test_entry_points_validate_before_launch():
+    lib = fdl.lib()
+    plan = _fake_plan()
+    null = None
+    # null plan
+    assert lib.fd_region_score(None, 64, 0x1000, 0x1000, 0x1000, 0x1000, 4096, None) == 1
+    # unsupported channel count
+    assert lib.fd_region_score(ctypes.byref(plan), 12, 0x1000, 0x1000, 0x1000, 0x1000, 4096, None) == 3
+    # workspace too small
+    need = lib.fd_region_score_ws_size(ctypes.byref(plan), 64)
+    assert need > 0
+    assert lib.fd_region_score(ctypes.byref(plan), 64, 0x1000, 0x1000, 0x1000, 0x1000, need - 1, None) == 2
+    # misaligned latent
+    assert lib.fd_region_score(ctypes.byref(plan), 64, 0x1004, 0x1000, 0x1000, 0x1000, need, None) == 1
+    # bad dims: D != H*dh, unsupported head dim
+    d_bad = fdl.FdDims(64, 1536, 24, 32, 6144)
+    assert lib.fd_block_ws_size(ctypes.byref(plan), ctypes.byref(d_bad)) > 0
+    w = fdl.FdBlockWeights(*([0x1000] * 10))
+    args = (0x1000, 0x1000, 0x1000, 0x1000, 0x1000, 0x1000, 0x1000, 0x1000, 1 << 40, None)
+    assert lib.fd_block_forward(ctypes.byref(plan), ctypes.byref(d_bad), ctypes.byref(w), *args) == 2
+    d_bad2 = fdl.FdDims(64, 96 * 2, 2, 96, 256)
+    assert lib.fd_block_forward(ctypes.byref(plan), ctypes.byref(d_bad2), ctypes.byref(w), *args) == 3
+    # block workspace too small
+    d = fdl.FdDims(64, 128, 2, 64, 256)
+    small = (0x1000, 0x1000, 0x1000, 0x1000, 0x1000, 0x1000, 0x1000, 0x1000, 1024, None)
+    assert lib.fd_block_forward(ctypes.byref(plan), ctypes.byref(d), ctypes.byref(w), *small) == 2
+    assert b"workspace" in lib.fd_last_error()
+    # null weight
+    w0 = fdl.FdBlockWeights(*([0x1000] * 9 + [0]))
+    assert lib.fd_block_forward(ctypes.byref(plan), ctypes.byref(d), ctypes.byref(w0), *args) == 1
+    # select: bad gate parameters, too many regions
+    g = fdl.FdGate(-1.0, 0)
+    assert lib.fd_select(ctypes.byref(plan), *([0x1000] * 2), g, *([0x1000] * 7), None) == 1
+    big = fdl.FdPlan(10000, 5000, 1, 2, 10000, *([0x1000] * 6))
+    assert lib.fd_select(ctypes.byref(big), *([0x1000] * 2), fdl.FdGate(0.0, 0), *([0x1000] * 7), None) == 3
+    # scatter: unknown skip mode
+    assert lib.fd_scatter_update(ctypes.byref(plan), 64, *([0x1000] * 7), 7, None) == 1
+
+
+def test_block_workspace_size_formula():
+    plan = fdl.FdPlan(4096, 64, 1, 64, 4096, *([0x1000] * 6))
+    d = fdl.FdDims(64, 1536, 24, 64, 6144)
+    got = fdl.lib().fd_block_ws_size(ctypes.byref(plan), ctypes.byref(d))
+    want = 6 * 1536 * 4 + 3 * 4096 * 1536 * 2 + 4096 * 6144 * 2
+    assert want <= got < want + 5 * 256
