@@ -281,6 +281,7 @@ class SparseStep:
         self.s_tilde = torch.zeros(R, dtype=torch.float64, device=dev)
         self.skip_run = torch.zeros(R, dtype=torch.int32, device=dev)
         self.active = torch.ones(R, dtype=torch.uint8, device=dev)
+        self.all_active = torch.ones(R, dtype=torch.uint8, device=dev)
         self.idx = torch.zeros(N, dtype=torch.int32, device=dev)
         self.cu_q = torch.zeros(B + 1, dtype=torch.int32, device=dev)
         self.m = torch.zeros(1, dtype=torch.int32, device=dev)
@@ -301,12 +302,14 @@ class SparseStep:
     def step(self, x: torch.Tensor, x_prev: torch.Tensor, eps: torch.Tensor, dt: torch.Tensor,
              cond: torch.Tensor, eta: float = 0.0, max_skip: int = 0, skip_mode: int = FD_SKIP_FREEZE,
              stateless: bool = False, stream=None) -> None:
-        """One step on the latent x (updated in place); eps fp64 [B], dt fp32 [B], cond fp32 [B, D]."""
+        """One step on the latent x (updated in place); eps fp64 [B], dt fp32 [B], cond fp32 [B, D].
+
+        stateless=True gates on fresh scores only (every region counts as
+        executed at the previous step)."""
         p, d, C = self.plan, self.d, self.d.C
-        if stateless:
-            self.active.fill_(1)
+        prev = self.all_active if stateless else self.active
         fd_region_score(p, C, x, x_prev, self.score, self.ws_score, stream)
-        fd_select(p, self.score, eps, eta, max_skip, self.s_tilde, self.skip_run, self.active, self.active,
+        fd_select(p, self.score, eps, eta, max_skip, self.s_tilde, self.skip_run, prev, self.active,
                   self.idx, self.cu_q, self.m, stream)
         fd_gather(p, C, x, self.idx, self.m, self.xa, stream)
         fd_embed(p, d, self.xa, self.params["w_e"], self.params["b_e"], self.params["pos"], self.idx, self.m,
