@@ -37,6 +37,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--pool", type=int, default=4, help="distinct latent pairs cycled through")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--workload", default=WORKLOAD, help="image (default), video, audio, packed or tiny")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU oracle sample")
     return ap.parse_args()
 
@@ -124,7 +125,7 @@ def main():
         print(json.dumps({"error": "no GPU visible"}))
         return 2
     torch.cuda.set_device(0)
-    w = wl.WORKLOADS[WORKLOAD]
+    w = wl.WORKLOADS[args.workload]
     rm = wl.region_map(w)
     print(f"[bench] workload {w.name}: N={w.N} R={w.R} D={w.D} L={w.L}; drawing inputs on the GPU",
           file=sys.stderr, flush=True)
@@ -180,6 +181,7 @@ def main():
     last = (args.warmup + args.steps - 1) % args.pool
     assert M == expected_m[last], f"active rows {M} != designed {expected_m[last]}"
     m_mean = float(np.mean([expected_m[(args.warmup + i) % args.pool] for i in range(args.steps)]))
+    regions_mean = m_mean * w.R / w.N
     ms_step = ms_total / args.steps
     dom_avg_ms = float(np.mean(dom_ms))
     achieved = kernel_flops(dominant, w, M) / (dom_avg_ms * 1e-3) / 1e12
@@ -190,7 +192,7 @@ def main():
         "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": w.description, "tokens": w.N, "active_tokens": m_mean, "regions": w.R,
-                   "active_regions": m_mean / 64, "blocks": w.L, "hidden": w.D, "heads": w.H, "head_dim": w.dh,
+                   "active_regions": regions_mean, "blocks": w.L, "hidden": w.D, "heads": w.H, "head_dim": w.dh,
                    "mlp": w.F, "latent_channels": w.C, "gate": "stateless, eps at the designed gap",
                    "parallelism": "single GPU"},
         "step_mfma_frac": step_flops(w, M) / (ms_step * 1e-3) / (PEAK_BF16_TFLOPS * 1e12),

@@ -46,10 +46,12 @@ FD_DEVICE int row_request(const int32_t* __restrict__ cu_q, int B, int i) {
   return b;
 }
 
+// GELU, tanh form: z/2 (1 + tanh(u)), u = sqrt(2/pi) (z + 0.044715 z^3).  Uses the
+// identity (1 + tanh(u)) / 2 = 1 / (1 + exp(-2u)), i.e. one exponential and one division.
 FD_DEVICE float gelu_tanh(float z) {
-  const float k0 = 0.7978845608028654f;  // sqrt(2/pi)
-  const float u = k0 * (z + 0.044715f * z * z * z);
-  return 0.5f * z * (1.0f + tanhf(u));
+  const float k2 = 1.5957691216057308f;  // 2 sqrt(2/pi)
+  const float t = k2 * (z + 0.044715f * z * z * z);
+  return z / (1.0f + __expf(-t));
 }
 
 }  // namespace fd
@@ -80,7 +82,7 @@ hipError_t launch_scatter_update(const fd_plan* p, int C, float* x, const float*
                                  const int32_t* m, const float* dt, float* vcache, const uint8_t* active,
                                  int skip_mode, hipStream_t s);
 hipError_t launch_adaln(const uint16_t* w, const float* b, const float* cond, int B, int D, int n_out,
-                        float* mod, hipStream_t s);
+                        float* mod, int32_t* zero_ints, int n_zero, hipStream_t s);
 hipError_t launch_ln_modulate(const float* h, const int32_t* cu_q, int B, const int32_t* m, int n_max, int D,
                               const float* mod, int mod_stride, int shift_off, int scale_off, uint16_t* a,
                               hipStream_t s);
@@ -103,7 +105,12 @@ struct GemmArgs {
   float* out_f32;        // RESID: h [M][N] (+=); EMBED: h [M][N]; OUT: v [M][N]
   const float* gate; int gate_stride;          // RESID: gate row per request
   const float* pos;      // EMBED: [N_tok][N]
+  // split-K scratch (tiled kernel): fp32 partial tiles and per-tile arrival counters
+  float* partial; int32_t* counters; int max_units;
 };
+// Bytes of split-K scratch the tiled GEMM needs (partials + counters), for any shape.
+size_t gemm_scratch_bytes();
+int gemm_max_tiles();
 hipError_t launch_gemm(GemmKind kind, const GemmArgs& a, hipStream_t s);
 
 hipError_t launch_attention(const uint16_t* q, const uint16_t* kc, const uint16_t* vc, uint16_t* o, int D, int H,

@@ -2,29 +2,33 @@
 //
 // C[M][N] = A[M][K] * B[N][K]^T, A = activations (bf16, row-major), B = weights
 // ([out][in] bf16), fp32 accumulation on v_mfma_f32_32x32x16_bf16.  M (the number
-// of active rows) lives on the device; the kernel is persistent: each workgroup
-// walks tiles blockIdx.x, blockIdx.x + gridDim.x, ... while they exist for the
-// current M, so the launch needs no host-side M.
+// of active rows) lives on the device, so both kernels are persistent: each
+// workgroup walks work units blockIdx.x, blockIdx.x + gridDim.x, ... that exist
+// for the current M, and the launch needs no host-side M.
 //
-// Tiling: 128x128 workgroup tile, BK = 64, 4 waves in a 2x2 grid, each wave a
-// 64x64 sub-tile of 2x2 MFMA 32x32 blocks.  A and B tiles are staged in LDS,
-// double-buffered, as rows of eight 16-byte chunks with chunk c of row r stored
-// at c ^ (r & 7) so that the MFMA operand reads (8 consecutive rows, one chunk
-// each) hit distinct banks.  The next K-slice is fetched into registers while
-// the current one feeds the MFMAs.
+// Tiled kernel (K % 64 == 0): 256x128 workgroup tile, BK = 64, 4 waves in a 2x2
+// grid, each wave a 128x64 sub-tile (4x2 MFMA 32x32 blocks).  Tiles stream from
+// HBM straight into LDS (buffer_load ... lds, 16 bytes per lane) through a
+// 3-stage ring, one barrier per K-step.  In LDS every tile row is eight 16-byte
+// chunks with chunk c of row r stored at c ^ (r & 7); the per-lane global
+// addresses are permuted so that each wave's contiguous 1 KB LDS write lands in
+// that order.  Rows past M (or N) re-read the last valid row; their results are
+// never stored.
+//
+// Split-K: when the tile count leaves most CUs idle, every tile's K range is cut
+// into S contiguous splits (S chosen on the device from M).  Each split stores
+// its fp32 tile to scratch and bumps the tile's arrival counter; the last split
+// to arrive sums all S partials in split order (deterministic) and runs the
+// epilogue, then resets the counter for the next launch.
+//
+// Work units are dealt to the 8 XCDs in contiguous chunks of tile order (a WG
+// runs on XCD blockIdx.x % 8), so the tiles one XCD runs concurrently share A
+// and B rows in its L2.
 #include "fd_common.h"
 
 namespace {
 
-constexpr int BM = 128, BN = 128, BK = 64;
-constexpr int kThreads = 256;
-constexpr int kChunks = BK / 8;                         // 16-byte chunks per tile row
-constexpr int kLoadsA = BM * kChunks / kThreads;        // 4
-constexpr int kLoadsB = BN * kChunks / kThreads;        // 4
-
-struct Frag {
-  f32x16_t c[2][2];
-};
+constexpr int kXcds = 8;
 
 template <int KIND>
 FD_DEVICE void epilogue(const fdh::GemmArgs& g, int row, int col, float acc) {
@@ -53,8 +57,345 @@ FD_DEVICE void epilogue(const fdh::GemmArgs& g, int row, int col, float acc) {
   }
 }
 
+// Epilogue on 8 consecutive columns col..col+7 of one output row (col % 8 == 0,
+// col + 8 <= N): v holds the fp32 accumulators.  Vector loads and stores only.
 template <int KIND>
-__global__ __launch_bounds__(kThreads, 2) void gemm_bf16_kernel(fdh::GemmArgs g) {
+FD_DEVICE void epilogue8(const fdh::GemmArgs& g, int row, int col, float v[8]) {
+  const float4 b0 = *reinterpret_cast<const float4*>(g.bias + col);
+  const float4 b1 = *reinterpret_cast<const float4*>(g.bias + col + 4);
+  v[0] += b0.x; v[1] += b0.y; v[2] += b0.z; v[3] += b0.w;
+  v[4] += b1.x; v[5] += b1.y; v[6] += b1.z; v[7] += b1.w;
+  if constexpr (KIND == fdh::GEMM_QKV || KIND == fdh::GEMM_GELU) {
+    if constexpr (KIND == fdh::GEMM_GELU) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = fd::gelu_tanh(v[e]);
+    }
+    uint4 o;
+    o.x = fd::pack_bf2(v[0], v[1]);
+    o.y = fd::pack_bf2(v[2], v[3]);
+    o.z = fd::pack_bf2(v[4], v[5]);
+    o.w = fd::pack_bf2(v[6], v[7]);
+    uint16_t* dst;
+    if constexpr (KIND == fdh::GEMM_QKV) {
+      const int D = g.D;
+      if (col < D) {
+        dst = g.out_bf16 + static_cast<size_t>(row) * D + col;
+      } else {
+        const size_t tok = static_cast<size_t>(g.idx[row]);
+        dst = (col < 2 * D) ? g.k_cache + tok * D + (col - D) : g.v_cache + tok * D + (col - 2 * D);
+      }
+    } else {
+      dst = g.out_bf16 + static_cast<size_t>(row) * g.N + col;
+    }
+    *reinterpret_cast<uint4*>(dst) = o;
+  } else {
+    float* hp = g.out_f32 + static_cast<size_t>(row) * g.N + col;
+    float4 r0, r1;
+    if constexpr (KIND == fdh::GEMM_RESID) {
+      const int b = fd::row_request(g.cu_q, g.n_req, row);
+      const float* gp = g.gate + static_cast<size_t>(b) * g.gate_stride + col;
+      const float4 g0 = *reinterpret_cast<const float4*>(gp);
+      const float4 g1 = *reinterpret_cast<const float4*>(gp + 4);
+      const float4 h0 = *reinterpret_cast<const float4*>(hp);
+      const float4 h1 = *reinterpret_cast<const float4*>(hp + 4);
+      r0 = make_float4(h0.x + g0.x * v[0], h0.y + g0.y * v[1], h0.z + g0.z * v[2], h0.w + g0.w * v[3]);
+      r1 = make_float4(h1.x + g1.x * v[4], h1.y + g1.y * v[5], h1.z + g1.z * v[6], h1.w + g1.w * v[7]);
+    } else if constexpr (KIND == fdh::GEMM_EMBED) {
+      const float* pp = g.pos + static_cast<size_t>(g.idx[row]) * g.N + col;
+      const float4 p0 = *reinterpret_cast<const float4*>(pp);
+      const float4 p1 = *reinterpret_cast<const float4*>(pp + 4);
+      r0 = make_float4(v[0] + p0.x, v[1] + p0.y, v[2] + p0.z, v[3] + p0.w);
+      r1 = make_float4(v[4] + p1.x, v[5] + p1.y, v[6] + p1.z, v[7] + p1.w);
+    } else {
+      r0 = make_float4(v[0], v[1], v[2], v[3]);
+      r1 = make_float4(v[4], v[5], v[6], v[7]);
+    }
+    reinterpret_cast<float4*>(hp)[0] = r0;
+    reinterpret_cast<float4*>(hp)[1] = r1;
+  }
+}
+
+// ---------------------------------------------------------------- tiled kernel
+
+// Workgroup tile BM x BN, WM x WN waves (each a (BM/WM) x (BN/WN) sub-tile of
+// 32x32 MFMA blocks), STAGES-deep LDS ring, OCC workgroups per CU.
+template <int BM_, int BN_, int WM_, int WN_, int STAGES_, int OCC_>
+struct TileCfg {
+  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, STAGES = STAGES_, OCC = OCC_;
+  static constexpr int WAVES = WM * WN, THREADS = WAVES * 64;
+  static constexpr int TM = BM / WM, TN = BN / WN, FM = TM / 32, FN = TN / 32;
+  static constexpr int CHUNKS = (BM + BN) * 8;              // 16-byte chunks per stage
+  static constexpr int LOADS = (BM + BN) / 8 / WAVES;       // 8-row wave-loads per wave per stage
+  static_assert((BM + BN) % (8 * WAVES) == 0, "tile rows must split into 8-row wave-loads");
+  static_assert(TM % 32 == 0 && TN % 32 == 0, "wave tile must be whole 32x32 MFMA blocks");
+};
+
+#ifndef FD_GEMM_CFG
+#define FD_GEMM_CFG 2
+#endif
+#if FD_GEMM_CFG == 0
+using Cfg = TileCfg<256, 128, 2, 2, 3, 1>;
+#elif FD_GEMM_CFG == 1
+using Cfg = TileCfg<256, 128, 4, 2, 3, 1>;
+#elif FD_GEMM_CFG == 2
+using Cfg = TileCfg<128, 128, 2, 2, 2, 2>;
+#else
+using Cfg = TileCfg<256, 256, 2, 4, 2, 1>;
+#endif
+
+constexpr int TBK = 64;
+#ifndef FD_GEMM_MAX_SPLIT
+#define FD_GEMM_MAX_SPLIT 16
+#endif
+constexpr int kMaxSplit = FD_GEMM_MAX_SPLIT;
+
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+typedef int int32x4_t __attribute__((ext_vector_type(4)));
+
+// Buffer resource of a raw byte buffer (base, no stride, 2^31-1 bytes in range).
+FD_DEVICE int32x4_t buffer_rsrc(const void* base) {
+  const uint64_t p = reinterpret_cast<uint64_t>(base);
+  int32x4_t r;
+  r.x = static_cast<int>(static_cast<uint32_t>(p));
+  r.y = static_cast<int>(static_cast<uint32_t>(p >> 32) & 0xffffu);
+  r.z = 0x7fffffff;
+  r.w = 0x00020000;
+  return r;
+}
+
+// 16 bytes per lane from buffer offset `voff` into LDS at lds_addr + 16 * lane
+// (lds_addr wave-uniform).  Issued as inline assembly so that the compiler does
+// not wait for it before unrelated LDS reads; completion is awaited explicitly
+// with s_waitcnt vmcnt before the barrier that publishes a stage.
+FD_DEVICE void lds_dma16(uint32_t lds_addr, uint32_t voff, int32x4_t rsrc) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds"
+               :
+               : "s"(lds_addr), "v"(voff), "s"(rsrc));
+}
+
+// Wait until at most N of this wave's vector-memory operations are in flight,
+// then barrier (no memory fence, so younger loads stay in flight).
+template <int N>
+FD_DEVICE void wait_vm_barrier() {
+  asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" : : "n"(N) : "memory");
+}
+
+FD_DEVICE float split_eff(int units, int cus) {
+  const int waves = (units + cus - 1) / cus;
+  return static_cast<float>(units) / static_cast<float>(waves * cus);
+}
+
+// Number of K splits for `tiles` output tiles and `nk` K-steps (identical in every WG).
+FD_DEVICE int choose_split(int tiles, int nk, int slots, int max_units) {
+  int best = 1;
+  float best_e = split_eff(tiles, slots);
+  for (int s = 2; s <= kMaxSplit; ++s) {
+    if (nk < 4 * s || tiles * s > max_units) break;
+    const float e = split_eff(tiles * s, slots) - 0.05f * static_cast<float>(s - 1);
+    if (e > best_e + 1e-6f) {
+      best_e = e;
+      best = s;
+    }
+  }
+  return best;
+}
+
+template <int KIND>
+__global__ __launch_bounds__(Cfg::THREADS, Cfg::OCC) void gemm_tiled_kernel(fdh::GemmArgs g, int slots) {
+  constexpr int BM = Cfg::BM, BN = Cfg::BN, FM = Cfg::FM, FN = Cfg::FN, TM = Cfg::TM, TN = Cfg::TN;
+  constexpr int WAVES = Cfg::WAVES, THREADS = Cfg::THREADS, LOADS = Cfg::LOADS, STAGES = Cfg::STAGES;
+  // the K-loop ring; after the loop it holds the fp32 output tile (row stride OSTRIDE)
+  constexpr int OSTRIDE = BN + 4;
+  constexpr int RING_U4 = STAGES * Cfg::CHUNKS;
+  constexpr int OUT_U4 = BM * OSTRIDE / 4;
+  __shared__ uint4 ring_mem[RING_U4 > OUT_U4 ? RING_U4 : OUT_U4];
+  uint4 (*ring)[Cfg::CHUNKS] = reinterpret_cast<uint4 (*)[Cfg::CHUNKS]>(ring_mem);
+  __shared__ int s_last;
+  const int M = min(*g.m, g.n_max);
+  if (M <= 0) return;
+  const int N = g.N, K = g.K;
+  const int tiles_m = (M + BM - 1) / BM;
+  const int tiles_n = (N + BN - 1) / BN;
+  const int tiles = tiles_m * tiles_n;
+  const int nk = K / TBK;
+  const int S = choose_split(tiles, nk, slots, g.max_units);
+  const int units = tiles * S;
+  const int per_xcd = (units + kXcds - 1) / kXcds;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / Cfg::WN, wn = wave % Cfg::WN;
+  const int l32 = lane & 31, lg = lane >> 5;
+  // this lane's chunk within every 8-row wave-load: row (lane >> 3), logical chunk (lane & 7) ^ (lane >> 3)
+  const int ld_row = lane >> 3;
+  const int ld_chunk = (lane & 7) ^ (lane >> 3);
+  const int32x4_t rs_a = buffer_rsrc(g.act);
+  const int32x4_t rs_b = buffer_rsrc(g.wt);
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  const uint32_t ring_base = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_ptr_t)&ring[0][0]));
+
+  for (int u = blockIdx.x; u < per_xcd * kXcds; u += gridDim.x) {
+    const int v = (u % kXcds) * per_xcd + u / kXcds;
+    if (v >= units) continue;
+    const int tile = v / S, split = v - (v / S) * S;
+    const int tm = tile % tiles_m, tn = tile / tiles_m;
+    const int m0 = tm * BM, n0 = tn * BN;
+    const int kt0 = (split * nk) / S, kt1 = ((split + 1) * nk) / S;
+
+    // per-lane byte offsets of this lane's rows for each of its wave-loads (k = 0)
+    uint32_t off[LOADS];
+#pragma unroll
+    for (int q = 0; q < LOADS; ++q) {
+      const int blk = wave + WAVES * q;        // 8-row block in the concatenated A|B tile
+      const int r = blk * 8 + ld_row;
+      const int gr = (blk * 8 < BM) ? min(m0 + r, M - 1) : min(n0 + (r - BM), N - 1);
+      off[q] = static_cast<uint32_t>((static_cast<size_t>(gr) * K + ld_chunk * 8) * 2);
+    }
+    auto issue = [&](int kt, int st) {
+      const uint32_t buf = ring_base + static_cast<uint32_t>(st * Cfg::CHUNKS * 16);
+      const uint32_t kb = static_cast<uint32_t>(kt * TBK * 2);
+#pragma unroll
+      for (int q = 0; q < LOADS; ++q) {
+        const uint32_t dst = buf + static_cast<uint32_t>((wave_u + WAVES * q) * 64 * 16);
+        if ((wave + WAVES * q) * 8 < BM)
+          lds_dma16(dst, off[q] + kb, rs_a);
+        else
+          lds_dma16(dst, off[q] + kb, rs_b);
+      }
+    };
+
+    f32x16_t acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+
+    const int nkt = kt1 - kt0;
+#pragma unroll
+    for (int p = 0; p < STAGES - 1; ++p)
+      if (p < nkt) issue(kt0 + p, p);
+    for (int it = 0; it < nkt; ++it) {
+      // stage `it` is complete once at most the younger stages' loads are in flight
+      const int younger = min(STAGES - 2, nkt - 1 - it);
+      if (younger >= 2) wait_vm_barrier<2 * LOADS>();
+      else if (younger == 1) wait_vm_barrier<LOADS>();
+      else wait_vm_barrier<0>();
+      if (it + STAGES - 1 < nkt) issue(kt0 + it + STAGES - 1, (it + STAGES - 1) % STAGES);
+      const uint4* sm = ring[it % STAGES];
+      bf16x8_t a[2][FM], b[2][FN];
+      auto frag = [&](int ks, int slot) {
+        const int ch = ks * 2 + lg;
+#pragma unroll
+        for (int i = 0; i < FM; ++i) {
+          const int row = wm * TM + i * 32 + l32;
+          a[slot][i] = __builtin_bit_cast(bf16x8_t, sm[row * 8 + (ch ^ (row & 7))]);
+        }
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+          const int row = BM + wn * TN + j * 32 + l32;
+          b[slot][j] = __builtin_bit_cast(bf16x8_t, sm[row * 8 + (ch ^ (row & 7))]);
+        }
+      };
+      frag(0, 0);
+#pragma unroll
+      for (int ks = 0; ks < TBK / 16; ++ks) {
+        if (ks + 1 < TBK / 16) frag(ks + 1, (ks + 1) & 1);
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+          for (int j = 0; j < FN; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ks & 1][i], b[ks & 1][j], acc[i][j], 0, 0, 0);
+      }
+    }
+    __syncthreads();   // every wave is done with the ring before the next unit refills it
+
+    if (S > 1) {
+      // Store this split's tile (lane-major: element e of thread t at e * THREADS + t)
+      // with device-coherent stores (they bypass the XCD-private L2, so no L2
+      // write-back fence is needed), wait for them, then count the arrival.
+      float* slot = g.partial + static_cast<size_t>(v) * (BM * BN) + tid;
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            __hip_atomic_store(slot + ((i * FN + j) * 16 + r) * THREADS, acc[i][j][r], __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      __syncthreads();
+      if (tid == 0) {
+        const int prev = __hip_atomic_fetch_add(&g.counters[tile], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        s_last = (prev == S - 1);
+        if (prev == S - 1) __hip_atomic_store(&g.counters[tile], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+      __syncthreads();
+      if (!s_last) continue;
+      // Sum the S partials (this split's included) in split order with
+      // device-coherent loads: the result does not depend on which split arrived last.
+      const float* base = g.partial + static_cast<size_t>(tile) * S * (BM * BN) + tid;
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            acc[i][j][r] = __hip_atomic_load(base + ((i * FN + j) * 16 + r) * THREADS, __ATOMIC_RELAXED,
+                                             __HIP_MEMORY_SCOPE_AGENT);
+      for (int s2 = 1; s2 < S; ++s2) {
+        const float* ps = base + static_cast<size_t>(s2) * (BM * BN);
+#pragma unroll
+        for (int i = 0; i < FM; ++i)
+#pragma unroll
+          for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+              acc[i][j][r] += __hip_atomic_load(ps + ((i * FN + j) * 16 + r) * THREADS, __ATOMIC_RELAXED,
+                                                __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+
+    // Stage the fp32 tile in LDS (accumulator layout of a 32x32 block: lane holds
+    // column l32, rows 8*(r/4) + 4*lg + (r%4)), then every thread finishes runs
+    // of 8 consecutive columns of a row with vector loads and stores.
+    float* otile = reinterpret_cast<float*>(ring_mem);
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int row = wm * TM + i * 32 + 8 * (r >> 2) + 4 * lg + (r & 3);
+          otile[row * OSTRIDE + wn * TN + j * 32 + l32] = acc[i][j][r];
+        }
+    __syncthreads();
+    constexpr int RUNS = BM * (BN / 8);
+#pragma unroll 4
+    for (int c = tid; c < RUNS; c += THREADS) {
+      const int lr = c / (BN / 8), lc = (c % (BN / 8)) * 8;
+      const int row = m0 + lr, col = n0 + lc;
+      if (row < M && col < N) {
+        const float4 x0 = *reinterpret_cast<const float4*>(otile + lr * OSTRIDE + lc);
+        const float4 x1 = *reinterpret_cast<const float4*>(otile + lr * OSTRIDE + lc + 4);
+        float v[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+        epilogue8<KIND>(g, row, col, v);
+      }
+    }
+    __syncthreads();   // the tile area is the next unit's ring
+  }
+}
+
+// ---------------------------------------------------------------- simple kernel (any K % 8 == 0)
+
+constexpr int BM = 128, BN = 128, BK = 64;
+constexpr int kThreads = 256;
+constexpr int kChunks = BK / 8;
+constexpr int kLoadsA = BM * kChunks / kThreads;
+constexpr int kLoadsB = BN * kChunks / kThreads;
+
+template <int KIND>
+__global__ __launch_bounds__(kThreads, 2) void gemm_simple_kernel(fdh::GemmArgs g) {
   __shared__ uint4 smem[2][(BM + BN) * kChunks];
   const int M = min(*g.m, g.n_max);
   const int N = g.N, K = g.K;
@@ -101,13 +442,13 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_bf16_kernel(fdh::GemmArgs g)
       }
     };
 
-    Frag acc;
+    f32x16_t acc[2][2];
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
       for (int j = 0; j < 2; ++j)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) acc.c[i][j][r] = 0.f;
+        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
     load(0);
     store(0);
@@ -134,14 +475,12 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_bf16_kernel(fdh::GemmArgs g)
         for (int i = 0; i < 2; ++i)
 #pragma unroll
           for (int j = 0; j < 2; ++j)
-            acc.c[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc.c[i][j], 0, 0, 0);
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
       }
       if (more) store(s ^ 1);
       __syncthreads();
     }
 
-    // Accumulator layout of a 32x32 block: lane holds column l32 and rows
-    // 8*(r/4) + 4*lg + (r%4), r = 0..15.
 #pragma unroll
     for (int i = 0; i < 2; ++i) {
 #pragma unroll
@@ -151,7 +490,7 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_bf16_kernel(fdh::GemmArgs g)
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
           const int col = n0 + wn * 64 + j * 32 + l32;
-          if (col < N) epilogue<KIND>(g, row, col, acc.c[i][j][r]);
+          if (col < N) epilogue<KIND>(g, row, col, acc[i][j][r]);
         }
       }
     }
@@ -162,16 +501,41 @@ __global__ __launch_bounds__(kThreads, 2) void gemm_bf16_kernel(fdh::GemmArgs g)
 
 namespace fdh {
 
+int gemm_max_tiles() { return 4 * num_cus(); }
+
+size_t gemm_scratch_bytes() {
+  const size_t units = static_cast<size_t>(gemm_max_tiles());
+  return units * Cfg::BM * Cfg::BN * sizeof(float) + units * sizeof(int32_t);
+}
+
 hipError_t launch_gemm(GemmKind kind, const GemmArgs& a, hipStream_t s) {
+  if (a.K % TBK == 0) {
+    const int slots = num_cus() * Cfg::OCC;
+    GemmArgs g = a;
+    if (!g.partial || !g.counters) g.max_units = 0;   // no scratch: never split
+    const long long tiles_max =
+        static_cast<long long>((a.n_max + Cfg::BM - 1) / Cfg::BM) * ((a.N + Cfg::BN - 1) / Cfg::BN);
+    long long grid = tiles_max * kMaxSplit;
+    if (grid > slots) grid = slots;
+    grid = ((grid + kXcds - 1) / kXcds) * kXcds;
+    switch (kind) {
+      case GEMM_QKV: gemm_tiled_kernel<GEMM_QKV><<<grid, Cfg::THREADS, 0, s>>>(g, slots); break;
+      case GEMM_RESID: gemm_tiled_kernel<GEMM_RESID><<<grid, Cfg::THREADS, 0, s>>>(g, slots); break;
+      case GEMM_GELU: gemm_tiled_kernel<GEMM_GELU><<<grid, Cfg::THREADS, 0, s>>>(g, slots); break;
+      case GEMM_EMBED: gemm_tiled_kernel<GEMM_EMBED><<<grid, Cfg::THREADS, 0, s>>>(g, slots); break;
+      case GEMM_OUT: gemm_tiled_kernel<GEMM_OUT><<<grid, Cfg::THREADS, 0, s>>>(g, slots); break;
+    }
+    return hipGetLastError();
+  }
   const long long tiles = static_cast<long long>((a.n_max + BM - 1) / BM) * ((a.N + BN - 1) / BN);
   const long long cap = 2LL * num_cus();
   const int grid = static_cast<int>(tiles < cap ? (tiles < 1 ? 1 : tiles) : cap);
   switch (kind) {
-    case GEMM_QKV: gemm_bf16_kernel<GEMM_QKV><<<grid, kThreads, 0, s>>>(a); break;
-    case GEMM_RESID: gemm_bf16_kernel<GEMM_RESID><<<grid, kThreads, 0, s>>>(a); break;
-    case GEMM_GELU: gemm_bf16_kernel<GEMM_GELU><<<grid, kThreads, 0, s>>>(a); break;
-    case GEMM_EMBED: gemm_bf16_kernel<GEMM_EMBED><<<grid, kThreads, 0, s>>>(a); break;
-    case GEMM_OUT: gemm_bf16_kernel<GEMM_OUT><<<grid, kThreads, 0, s>>>(a); break;
+    case GEMM_QKV: gemm_simple_kernel<GEMM_QKV><<<grid, kThreads, 0, s>>>(a); break;
+    case GEMM_RESID: gemm_simple_kernel<GEMM_RESID><<<grid, kThreads, 0, s>>>(a); break;
+    case GEMM_GELU: gemm_simple_kernel<GEMM_GELU><<<grid, kThreads, 0, s>>>(a); break;
+    case GEMM_EMBED: gemm_simple_kernel<GEMM_EMBED><<<grid, kThreads, 0, s>>>(a); break;
+    case GEMM_OUT: gemm_simple_kernel<GEMM_OUT><<<grid, kThreads, 0, s>>>(a); break;
   }
   return hipGetLastError();
 }

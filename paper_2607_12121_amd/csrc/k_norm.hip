@@ -15,9 +15,13 @@ constexpr int kAdaLdsFloats = 12288;    // 48 KB of SiLU(cond)
 __global__ __launch_bounds__(kAdaThreads) void adaln_gemv_kernel(const uint16_t* __restrict__ W,
                                                                  const float* __restrict__ bias,
                                                                  const float* __restrict__ cond, int B, int D,
-                                                                 int n_out, int b_chunk, float* __restrict__ mod) {
+                                                                 int n_out, int b_chunk, float* __restrict__ mod,
+                                                                 int32_t* __restrict__ zero_ints, int n_zero) {
   __shared__ float sc[kAdaLdsFloats];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  // The block's first kernel also clears the GEMM split-K arrival counters.
+  if (blockIdx.x == 0 && zero_ints)
+    for (int i = threadIdx.x; i < n_zero; i += kAdaThreads) zero_ints[i] = 0;
   const int row0 = blockIdx.x * kAdaRowsPerBlock + wave * kAdaRowsPerWave;
   for (int b0 = 0; b0 < B; b0 += b_chunk) {
     const int nb = min(b_chunk, B - b0);
@@ -143,11 +147,11 @@ __global__ __launch_bounds__(256) void ln_modulate_kernel(const float* __restric
 namespace fdh {
 
 hipError_t launch_adaln(const uint16_t* w, const float* b, const float* cond, int B, int D, int n_out, float* mod,
-                        hipStream_t s) {
+                        int32_t* zero_ints, int n_zero, hipStream_t s) {
   int b_chunk = kAdaLdsFloats / D;
   if (b_chunk > kAdaMaxB) b_chunk = kAdaMaxB;
   const int grid = (n_out + kAdaRowsPerBlock - 1) / kAdaRowsPerBlock;
-  adaln_gemv_kernel<<<grid, kAdaThreads, 0, s>>>(w, b, cond, B, D, n_out, b_chunk, mod);
+  adaln_gemv_kernel<<<grid, kAdaThreads, 0, s>>>(w, b, cond, B, D, n_out, b_chunk, mod, zero_ints, n_zero);
   return hipGetLastError();
 }
 

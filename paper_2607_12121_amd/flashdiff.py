@@ -16,7 +16,8 @@ from typing import Dict, Optional, Sequence
 import numpy as np
 import torch
 
-LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libflashdiff.so")
+LIB_PATH = os.environ.get("FLASHDIFF_LIB") or os.path.join(os.path.dirname(os.path.abspath(__file__)),
+                                                            "libflashdiff.so")
 
 FD_SKIP_FREEZE = 0
 FD_SKIP_REUSE_DRIFT = 1
