@@ -48,7 +48,9 @@ BlockWs carve_block_ws(const fd_plan* p, const fd_dims* d, void* base) {
   w.o = static_cast<uint16_t*>(take(n * d->D * 2));
   w.g = static_cast<uint16_t*>(take(n * d->F * 2));
   const size_t tiles = static_cast<size_t>(fdh::gemm_max_tiles());
-  w.partial = static_cast<float*>(take(fdh::gemm_scratch_bytes() - tiles * sizeof(int32_t)));
+  const size_t gemm_part = fdh::gemm_scratch_bytes() - tiles * sizeof(int32_t);
+  const size_t attn_part = fdh::attn_scratch_bytes(d->dh);
+  w.partial = static_cast<float*>(take(gemm_part > attn_part ? gemm_part : attn_part));
   w.counters = static_cast<int32_t*>(take(tiles * sizeof(int32_t)));
   w.bytes = off;
   return w;
@@ -310,7 +312,7 @@ fd_status fd_block_forward(const fd_plan* plan, const fd_dims* dims, const fd_bl
   FD_LAUNCH(FD_K_GEMM_QKV, s, fdh::launch_gemm(fdh::GEMM_QKV, g, s));
   FD_LAUNCH(FD_K_ATTN, s,
             fdh::launch_attention(bw.q, k_cache, v_cache, bw.o, D, dims->H, dims->dh, cu_q, plan->req_tok_off, B, N,
-                                  m, s));
+                                  plan->max_request_tokens, bw.partial, bw.counters, s));
   g = fdh::GemmArgs{};
   g.n_max = N; g.m = m; g.idx = idx; g.cu_q = cu_q; g.n_req = B; g.D = D;
   g.partial = bw.partial; g.counters = bw.counters; g.max_units = fdh::gemm_max_tiles();

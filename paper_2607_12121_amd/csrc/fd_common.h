@@ -115,6 +115,8 @@ hipError_t launch_gemm(GemmKind kind, const GemmArgs& a, hipStream_t s);
 
 hipError_t launch_attention(const uint16_t* q, const uint16_t* kc, const uint16_t* vc, uint16_t* o, int D, int H,
                             int dh, const int32_t* cu_q, const int32_t* req_tok_off, int B, int n_max,
-                            const int32_t* m, hipStream_t s);
+                            int max_req_tokens, float* partial, int32_t* counters, hipStream_t s);
+// Bytes of KV-split scratch the attention kernel needs for head dim dh.
+size_t attn_scratch_bytes(int dh);
 
 }  // namespace fdh
