@@ -39,6 +39,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--workload", default=WORKLOAD, help="image (default), video, audio, packed or tiny")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU oracle sample")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="launch a plain fp32 copy of this many MiB 3 times first (counter calibration)")
     return ap.parse_args()
 
 
@@ -61,6 +63,21 @@ def kernel_bytes(name: str, w, M: int) -> float:
 def step_flops(w, M: int) -> float:
     per_block = sum(kernel_flops(k, w, M) for k in ("gemm_qkv", "gemm_o", "gemm_mlp1", "gemm_mlp2", "attn"))
     return w.L * per_block + kernel_flops("embed", w, M) + kernel_flops("final", w, M)
+
+
+KERNEL_SOURCES = {"attn": ("k_attn.hip", "fd_common.h")}
+for _g in ("gemm_qkv", "gemm_o", "gemm_mlp1", "gemm_mlp2"):
+    KERNEL_SOURCES[_g] = ("k_gemm.hip", "fd_common.h")
+
+
+def traffic_per_launch(kernel: str, workload: str):
+    """HBM bytes per launch from the committed counter summary of this kernel and
+    workload, or None if there is none or the kernel's sources changed since."""
+    from paper_2607_12121_amd.rocprof_summary import read_traffic
+    srcs = [os.path.join(ROOT, "paper_2607_12121_amd", "csrc", f) for f in KERNEL_SOURCES.get(kernel, ())]
+    if not srcs:
+        return None
+    return read_traffic(os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.txt"), srcs)
 
 
 def cpu_baseline(w, params_gpu, M_expected: int, budget_s: float):
@@ -125,6 +142,13 @@ def main():
         print(json.dumps({"error": "no GPU visible"}))
         return 2
     torch.cuda.set_device(0)
+    if args.copy_probe_mib > 0:
+        src = torch.ones(args.copy_probe_mib << 18, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.neg(src, out=dst)
+        torch.cuda.synchronize()
+        del src, dst
     w = wl.WORKLOADS[args.workload]
     rm = wl.region_map(w)
     print(f"[bench] workload {w.name}: N={w.N} R={w.R} D={w.D} L={w.L}; drawing inputs on the GPU",
@@ -185,6 +209,7 @@ def main():
     ms_step = ms_total / args.steps
     dom_avg_ms = float(np.mean(dom_ms))
     achieved = kernel_flops(dominant, w, M) / (dom_avg_ms * 1e-3) / 1e12
+    traffic = traffic_per_launch(dominant, w.name)
     out = {
         "metric": "active tokens/sec per region-sparse DiT step; % bf16 MFMA peak",
         "value": m_mean / (ms_step * 1e-3),
@@ -197,7 +222,7 @@ def main():
                    "parallelism": "single GPU"},
         "step_mfma_frac": step_flops(w, M) / (ms_step * 1e-3) / (PEAK_BF16_TFLOPS * 1e12),
         "roofline": {"kernel": dominant, "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": None,
+                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": traffic,
                      "launches": len(dom_ms), "avg_ms": dom_avg_ms},
         "kernels_ms_per_step": {k: round(v[0], 4) for k, v in per_kernel.items()},
     }

@@ -19,8 +19,12 @@ constexpr int kWave = 64;
 // fp32 -> bf16 bits, round to nearest even (hardware conversion on gfx950).
 FD_DEVICE uint16_t f2bf(float x) { return __builtin_bit_cast(uint16_t, static_cast<__bf16>(x)); }
 FD_DEVICE float bf2f(uint16_t b) { return __uint_as_float(static_cast<uint32_t>(b) << 16); }
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+// two fp32 -> packed bf16 pair (lo in the low half), one v_cvt_pk_bf16_f32, round to nearest even
 FD_DEVICE uint32_t pack_bf2(float lo, float hi) {
-  return static_cast<uint32_t>(f2bf(lo)) | (static_cast<uint32_t>(f2bf(hi)) << 16);
+  const f32x2_t f = {lo, hi};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f, bf16x2_t));
 }
 
 FD_DEVICE float wave_sum(float v) {

@@ -1,0 +1,138 @@
+"""Short text summaries of rocprofv3 output, for the figures kept beside the code.
+
+    python -m paper_2607_12121_amd.rocprof_summary stats  <kernel_stats.csv> --title T --cmd C
+    python -m paper_2607_12121_amd.rocprof_summary traffic --fetch <fetch counter_collection.csv>
+        --write <write counter_collection.csv> --kernel REGEX --copy-kernel REGEX
+        --copy-bytes S --source FILE [FILE ...] --title T --cmd C [--cmd C ...]
+
+`stats` turns a `--kernel-trace --stats` kernel table into a markdown table.
+
+`traffic` turns two `--pmc` passes (FETCH_SIZE, then WRITE_SIZE; both in KiB per
+dispatch) into HBM bytes per launch of one kernel.  Each counter is scaled by
+what it reads for a plain copy kernel of S bytes launched in the same run (the
+copy reads S and writes S bytes), so the figure is in the copy's units.  The
+summary records the sha256 of the kernel's sources; a reader that finds other
+sources treats the figure as stale.
+"""
+from __future__ import annotations
+
+import argparse
+import csv
+import hashlib
+import os
+import re
+import sys
+from collections import defaultdict
+
+
+def source_digest(paths) -> str:
+    h = hashlib.sha256()
+    for p in sorted(paths):
+        h.update(os.path.basename(p).encode())
+        with open(p, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def _short(name: str) -> str:
+    s = name.replace("void ", "").replace("(anonymous namespace)::", "")
+    if s.startswith("at::"):
+        return "torch " + s.split("<")[0].split("(")[0]
+    return re.sub(r"\(.*$", "", s)
+
+
+def stats(path: str, title: str, cmds) -> str:
+    rows = list(csv.DictReader(open(path)))
+    out = [f"# {title}", "", "command (run from the repo root on an MI355X):", ""]
+    out += [f"    {c}" for c in cmds]
+    out += ["", "rocprofv3 kernel statistics, durations in microseconds", "",
+            "| kernel | calls | total us | avg us | min us | max us | % |", "|---|---|---|---|---|---|---|"]
+    for r in rows:
+        out.append(f"| {_short(r['Name'])[:72]} | {r['Calls']} | {float(r['TotalDurationNs']) / 1e3:.1f} | "
+                   f"{float(r['AverageNs']) / 1e3:.3f} | {float(r['MinNs']) / 1e3:.3f} | "
+                   f"{float(r['MaxNs']) / 1e3:.3f} | {float(r['Percentage']):.2f} |")
+    return "\n".join(out) + "\n"
+
+
+def _per_dispatch(path: str, counter: str, regex: str):
+    """{dispatch id: (counter value summed over its dimensions, duration ns)} of matching kernels."""
+    pat = re.compile(regex)
+    val = defaultdict(float)
+    dur = {}
+    for r in csv.DictReader(open(path)):
+        if r["Counter_Name"] != counter or not pat.search(r["Kernel_Name"]):
+            continue
+        val[r["Dispatch_Id"]] += float(r["Counter_Value"])
+        dur[r["Dispatch_Id"]] = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+    return {k: (val[k], dur[k]) for k in val}
+
+
+def traffic(a) -> str:
+    fetch = _per_dispatch(a.fetch, "FETCH_SIZE", a.kernel)
+    write = _per_dispatch(a.write, "WRITE_SIZE", a.kernel)
+    cf = _per_dispatch(a.fetch, "FETCH_SIZE", a.copy_kernel)
+    cw = _per_dispatch(a.write, "WRITE_SIZE", a.copy_kernel)
+    if not (fetch and write and cf and cw):
+        raise SystemExit("no matching dispatches for the kernel or the copy kernel")
+    kib = a.copy_bytes / 1024.0
+    # the largest of the copy's readings: its first launch may find part of the source in cache
+    f_scale = kib / max(v for v, _ in cf.values())
+    w_scale = kib / max(v for v, _ in cw.values())
+    f_kib = sum(v for v, _ in fetch.values()) / len(fetch)
+    w_kib = sum(v for v, _ in write.values()) / len(write)
+    bytes_per_launch = (f_kib * f_scale + w_kib * w_scale) * 1024.0
+    out = [f"# {a.title}", "", "commands (run from the repo root on an MI355X):", ""]
+    out += [f"    {c}" for c in a.cmd]
+    out += ["", f"kernel regex: `{a.kernel}`; copy kernel regex: `{a.copy_kernel}`, "
+                f"{a.copy_bytes} bytes read and written per copy launch", "",
+            "| figure | value |", "|---|---|",
+            f"| dispatches (fetch pass / write pass) | {len(fetch)} / {len(write)} |",
+            f"| FETCH_SIZE per dispatch, KiB | {f_kib:,.1f} |",
+            f"| WRITE_SIZE per dispatch, KiB | {w_kib:,.1f} |",
+            f"| copy FETCH_SIZE per dispatch, KiB (max of {len(cf)}) | {max(v for v, _ in cf.values()):,.1f} |",
+            f"| copy WRITE_SIZE per dispatch, KiB (max of {len(cw)}) | {max(v for v, _ in cw.values()):,.1f} |",
+            f"| fetch scale (copy bytes / copy counter) | {f_scale:.4f} |",
+            f"| write scale (copy bytes / copy counter) | {w_scale:.4f} |",
+            f"| HBM bytes read per launch (scaled) | {f_kib * f_scale * 1024:,.0f} |",
+            f"| HBM bytes written per launch (scaled) | {w_kib * w_scale * 1024:,.0f} |", "",
+            f"bytes_per_launch: {bytes_per_launch:.0f}",
+            f"source_sha256: {source_digest(a.source)}",
+            "sources: " + " ".join(os.path.relpath(p) for p in sorted(a.source))]
+    return "\n".join(out) + "\n"
+
+
+def read_traffic(path: str, sources):
+    """bytes_per_launch from a traffic summary, or None when it is missing or its
+    recorded sources differ from `sources` (the kernel changed since the counters)."""
+    if not os.path.exists(path):
+        return None
+    text = open(path).read()
+    m = re.search(r"^bytes_per_launch: (\d+)", text, re.M)
+    s = re.search(r"^source_sha256: ([0-9a-f]+)", text, re.M)
+    if not (m and s) or s.group(1) != source_digest(sources):
+        return None
+    return float(m.group(1))
+
+
+def main(argv=None):
+    ap = argparse.ArgumentParser()
+    sub = ap.add_subparsers(dest="what", required=True)
+    s = sub.add_parser("stats")
+    s.add_argument("csv")
+    s.add_argument("--title", required=True)
+    s.add_argument("--cmd", action="append", required=True)
+    t = sub.add_parser("traffic")
+    t.add_argument("--fetch", required=True)
+    t.add_argument("--write", required=True)
+    t.add_argument("--kernel", required=True)
+    t.add_argument("--copy-kernel", required=True)
+    t.add_argument("--copy-bytes", type=int, required=True)
+    t.add_argument("--source", nargs="+", required=True)
+    t.add_argument("--title", required=True)
+    t.add_argument("--cmd", action="append", required=True)
+    a = ap.parse_args(argv)
+    sys.stdout.write(stats(a.csv, a.title, a.cmd) if a.what == "stats" else traffic(a))
+
+
+if __name__ == "__main__":
+    main()
