@@ -99,6 +99,8 @@ typedef struct fd_block_weights {
   const uint16_t* w_1;   const float* b_1;     /* [F][D]                                     */
   const uint16_t* w_2;   const float* b_2;     /* [D][F]                                     */
   const uint16_t* w_ada; const float* b_ada;   /* [6D][D]: shift1|scale1|gate1|shift2|scale2|gate2 */
+  const float* mod;      /* optional [B][6D]: this block's modulation from fd_adaln; when
+                            non-null, w_ada, b_ada and cond are not read (may be null) */
 } fd_block_weights;
 
 /* Final layer (device): adaLN (shift | scale) [2D][D] and output projection [C][D]. */
@@ -187,6 +189,21 @@ fd_status fd_embed(const fd_plan* plan, const fd_dims* dims, const uint16_t* xa,
                    const float* b_e, const float* pos, const int32_t* idx, const int32_t* m,
                    float* h, fd_stream_t stream);
 
+/* ---------------------------------------------------------------- adaLN
+ * Modulation of n_blocks stacked blocks in one pass over their weights:
+ *   mod[l][b][j] = sum_k W[l][j][k] * SiLU(cond[b][k]) + bias[l][j],  j < n_out
+ * (the adaLN conditioning of the DiT blocks; it depends on cond only, so the
+ * modulation of every block of a step can be formed before the first block).
+ *   w_ada  device bf16 [n_blocks][n_out][D] (D = dims->D), 16-byte aligned
+ *   b_ada  device fp32 [n_blocks][n_out]
+ *   cond   device fp32 [n_requests][D], 16-byte aligned
+ *   mod    device fp32 [n_blocks][n_requests][n_out] (output)
+ * Errors: FD_E_ARG for null or misaligned pointers or non-positive counts.
+ */
+fd_status fd_adaln(const fd_dims* dims, int32_t n_blocks, int32_t n_out, int32_t n_requests,
+                   const uint16_t* w_ada, const float* b_ada, const float* cond, float* mod,
+                   fd_stream_t stream);
+
 /* ---------------------------------------------------------------- block
  * One adaLN DiT block on the active rows (Sec. 4 Backend: active patches run
  * with the K/V cache; Prop. "Stale-KV Perturbation"):
@@ -199,7 +216,7 @@ fd_status fd_embed(const fd_plan* plan, const fd_dims* dims, const uint16_t* xa,
  *   h  += gate1 * (o W_o^T + b_o)
  *   a   = bf16(LN(h) * (1 + scale2) + shift2)
  *   h  += gate2 * (GELU_tanh(a W_1^T + b_1) W_2^T + b_2)
- *   cond     device fp32 [B][D]
+ *   cond     device fp32 [B][D] (not read when w->mod is given)
  *   h        device fp32 [N][D], rows < *m updated in place
  *   idx, cu_q, m  from fd_select
  *   k_cache, v_cache  device bf16 [N][D] of this block (head h at columns h*dh..)

@@ -279,6 +279,19 @@ fd_status fd_embed(const fd_plan* plan, const fd_dims* dims, const uint16_t* xa,
   return FD_OK;
 }
 
+fd_status fd_adaln(const fd_dims* dims, int32_t n_blocks, int32_t n_out, int32_t n_requests, const uint16_t* w_ada,
+                   const float* b_ada, const float* cond, float* mod, fd_stream_t stream) {
+  FD_TRY(check_dims(dims));
+  FD_REQUIRE(w_ada && b_ada && cond && mod, "null pointer");
+  FD_REQUIRE(n_blocks >= 1 && n_out >= 1 && n_requests >= 1, "n_blocks, n_out and n_requests must be positive");
+  FD_REQUIRE(static_cast<long long>(n_blocks) * n_out <= (1LL << 28), "too many modulation rows");
+  FD_REQUIRE(aligned(w_ada, 16) && aligned(cond, 16), "misaligned buffer");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  FD_LAUNCH(FD_K_ADALN, s,
+            fdh::launch_adaln(w_ada, b_ada, cond, n_requests, dims->D, n_out, n_blocks, mod, nullptr, 0, s));
+  return FD_OK;
+}
+
 size_t fd_block_ws_size(const fd_plan* plan, const fd_dims* dims) {
   if (!plan || !dims) return 0;
   return carve_block_ws(plan, dims, nullptr).bytes;
@@ -289,21 +302,27 @@ fd_status fd_block_forward(const fd_plan* plan, const fd_dims* dims, const fd_bl
                            uint16_t* v_cache, void* ws, size_t ws_bytes, fd_stream_t stream) {
   FD_TRY(check_plan(plan));
   FD_TRY(check_dims(dims));
-  FD_REQUIRE(w && cond && h && idx && cu_q && m && k_cache && v_cache && ws, "null pointer");
-  FD_REQUIRE(w->w_qkv && w->b_qkv && w->w_o && w->b_o && w->w_1 && w->b_1 && w->w_2 && w->b_2 && w->w_ada &&
-                 w->b_ada,
+  FD_REQUIRE(w && h && idx && cu_q && m && k_cache && v_cache && ws, "null pointer");
+  FD_REQUIRE(w->w_qkv && w->b_qkv && w->w_o && w->b_o && w->w_1 && w->b_1 && w->w_2 && w->b_2 &&
+                 (w->mod || (w->w_ada && w->b_ada && cond)),
              "null weight pointer");
   FD_REQUIRE(aligned(w->w_qkv, 16) && aligned(w->w_o, 16) && aligned(w->w_1, 16) && aligned(w->w_2, 16) &&
-                 aligned(w->w_ada, 16) && aligned(h, 16) && aligned(k_cache, 16) && aligned(v_cache, 16) &&
-                 aligned(ws, kAlign),
+                 (w->mod ? aligned(w->mod, 16) : aligned(w->w_ada, 16)) && aligned(h, 16) && aligned(k_cache, 16) &&
+                 aligned(v_cache, 16) && aligned(ws, kAlign),
              "misaligned buffer");
   const BlockWs bw = carve_block_ws(plan, dims, ws);
   if (ws_bytes < bw.bytes) return fdh::set_error("block workspace too small (%zu < %zu)", ws_bytes, bw.bytes), FD_E_SHAPE;
   const int D = dims->D, F = dims->F, B = plan->n_requests, N = plan->n_tokens;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
 
-  FD_LAUNCH(FD_K_ADALN, s, fdh::launch_adaln(w->w_ada, w->b_ada, cond, B, D, 6 * D, bw.mod, bw.counters, fdh::gemm_max_tiles(), s));
-  FD_LAUNCH(FD_K_LN, s, fdh::launch_ln_modulate(h, cu_q, B, m, N, D, bw.mod, 6 * D, 0, D, bw.a, s));
+  // modulation: precomputed by fd_adaln, else computed here (that kernel then also clears the counters)
+  const float* mod = w->mod ? w->mod : bw.mod;
+  if (!w->mod)
+    FD_LAUNCH(FD_K_ADALN, s,
+              fdh::launch_adaln(w->w_ada, w->b_ada, cond, B, D, 6 * D, 1, bw.mod, bw.counters, fdh::gemm_max_tiles(), s));
+  FD_LAUNCH(FD_K_LN, s,
+            fdh::launch_ln_modulate(h, cu_q, B, m, N, D, mod, 6 * D, 0, D, bw.a, w->mod ? bw.counters : nullptr,
+                                    fdh::gemm_max_tiles(), s));
   fdh::GemmArgs g{};
   g.n_max = N; g.m = m; g.idx = idx; g.cu_q = cu_q; g.n_req = B; g.D = D;
   g.partial = bw.partial; g.counters = bw.counters; g.max_units = fdh::gemm_max_tiles();
@@ -317,9 +336,9 @@ fd_status fd_block_forward(const fd_plan* plan, const fd_dims* dims, const fd_bl
   g.n_max = N; g.m = m; g.idx = idx; g.cu_q = cu_q; g.n_req = B; g.D = D;
   g.partial = bw.partial; g.counters = bw.counters; g.max_units = fdh::gemm_max_tiles();
   g.act = bw.o; g.wt = w->w_o; g.bias = w->b_o; g.N = D; g.K = D;
-  g.out_f32 = h; g.gate = bw.mod + 2 * D; g.gate_stride = 6 * D;
+  g.out_f32 = h; g.gate = mod + 2 * D; g.gate_stride = 6 * D;
   FD_LAUNCH(FD_K_GEMM_O, s, fdh::launch_gemm(fdh::GEMM_RESID, g, s));
-  FD_LAUNCH(FD_K_LN, s, fdh::launch_ln_modulate(h, cu_q, B, m, N, D, bw.mod, 6 * D, 3 * D, 4 * D, bw.a, s));
+  FD_LAUNCH(FD_K_LN, s, fdh::launch_ln_modulate(h, cu_q, B, m, N, D, mod, 6 * D, 3 * D, 4 * D, bw.a, nullptr, 0, s));
   g = fdh::GemmArgs{};
   g.n_max = N; g.m = m; g.idx = idx; g.cu_q = cu_q; g.n_req = B; g.D = D;
   g.partial = bw.partial; g.counters = bw.counters; g.max_units = fdh::gemm_max_tiles();
@@ -329,7 +348,7 @@ fd_status fd_block_forward(const fd_plan* plan, const fd_dims* dims, const fd_bl
   g.n_max = N; g.m = m; g.idx = idx; g.cu_q = cu_q; g.n_req = B; g.D = D;
   g.partial = bw.partial; g.counters = bw.counters; g.max_units = fdh::gemm_max_tiles();
   g.act = bw.g; g.wt = w->w_2; g.bias = w->b_2; g.N = D; g.K = F;
-  g.out_f32 = h; g.gate = bw.mod + 5 * D; g.gate_stride = 6 * D;
+  g.out_f32 = h; g.gate = mod + 5 * D; g.gate_stride = 6 * D;
   FD_LAUNCH(FD_K_GEMM_MLP2, s, fdh::launch_gemm(fdh::GEMM_RESID, g, s));
   return FD_OK;
 }
@@ -346,8 +365,9 @@ fd_status fd_final(const fd_plan* plan, const fd_dims* dims, const fd_final_weig
   if (ws_bytes < bw.bytes) return fdh::set_error("final workspace too small"), FD_E_SHAPE;
   const int D = dims->D, B = plan->n_requests, N = plan->n_tokens;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  FD_LAUNCH(FD_K_ADALN, s, fdh::launch_adaln(w->w_ada, w->b_ada, cond, B, D, 2 * D, bw.mod, bw.counters, fdh::gemm_max_tiles(), s));
-  FD_LAUNCH(FD_K_LN, s, fdh::launch_ln_modulate(h, cu_q, B, m, N, D, bw.mod, 2 * D, 0, D, bw.a, s));
+  FD_LAUNCH(FD_K_ADALN, s,
+            fdh::launch_adaln(w->w_ada, w->b_ada, cond, B, D, 2 * D, 1, bw.mod, bw.counters, fdh::gemm_max_tiles(), s));
+  FD_LAUNCH(FD_K_LN, s, fdh::launch_ln_modulate(h, cu_q, B, m, N, D, bw.mod, 2 * D, 0, D, bw.a, nullptr, 0, s));
   fdh::GemmArgs g{};
   g.n_max = N; g.m = m; g.cu_q = cu_q; g.n_req = B;
   g.partial = bw.partial; g.counters = bw.counters; g.max_units = fdh::gemm_max_tiles();

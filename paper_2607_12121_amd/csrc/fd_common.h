@@ -57,6 +57,13 @@ FD_DEVICE float gelu_tanh(float z) {
   const float t = k2 * (z + 0.044715f * z * z * z);
   return z / (1.0f + __expf(-t));
 }
+// The same GELU with hardware exp2 and reciprocal (about 2 ulp): used in the MLP
+// epilogue, whose result is rounded to bf16 right after.
+FD_DEVICE float gelu_tanh_fast(float z) {
+  const float k2l = 2.302208198144325f;  // 2 sqrt(2/pi) log2(e)
+  const float t = k2l * (z + 0.044715f * z * z * z);
+  return z * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-t));
+}
 
 }  // namespace fd
 
@@ -85,11 +92,11 @@ hipError_t launch_gather(const fd_plan* p, int C, const float* x, const int32_t*
 hipError_t launch_scatter_update(const fd_plan* p, int C, float* x, const float* v, const int32_t* idx,
                                  const int32_t* m, const float* dt, float* vcache, const uint8_t* active,
                                  int skip_mode, hipStream_t s);
-hipError_t launch_adaln(const uint16_t* w, const float* b, const float* cond, int B, int D, int n_out,
+hipError_t launch_adaln(const uint16_t* w, const float* b, const float* cond, int B, int D, int n_out, int n_blocks,
                         float* mod, int32_t* zero_ints, int n_zero, hipStream_t s);
 hipError_t launch_ln_modulate(const float* h, const int32_t* cu_q, int B, const int32_t* m, int n_max, int D,
                               const float* mod, int mod_stride, int shift_off, int scale_off, uint16_t* a,
-                              hipStream_t s);
+                              int32_t* zero_ints, int n_zero, hipStream_t s);
 
 // GEMM epilogue kinds.
 enum GemmKind { GEMM_QKV = 0, GEMM_RESID = 1, GEMM_GELU = 2, GEMM_EMBED = 3, GEMM_OUT = 4 };

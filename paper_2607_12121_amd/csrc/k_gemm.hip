@@ -2,24 +2,32 @@
 //
 // C[M][N] = A[M][K] * B[N][K]^T, A = activations (bf16, row-major), B = weights
 // ([out][in] bf16), fp32 accumulation on v_mfma_f32_32x32x16_bf16.  M (the number
-// of active rows) lives on the device, so both kernels are persistent: each
-// workgroup walks work units blockIdx.x, blockIdx.x + gridDim.x, ... that exist
-// for the current M, and the launch needs no host-side M.
+// of active rows) lives on the device, so the kernels are persistent: each
+// workgroup walks the work units that exist for the current M, and the launch
+// needs no host-side M.
 //
-// Tiled kernel (K % 64 == 0): 256x128 workgroup tile, BK = 64, 4 waves in a 2x2
-// grid, each wave a 128x64 sub-tile (4x2 MFMA 32x32 blocks).  Tiles stream from
-// HBM straight into LDS (buffer_load ... lds, 16 bytes per lane) through a
-// 3-stage ring, one barrier per K-step.  In LDS every tile row is eight 16-byte
-// chunks with chunk c of row r stored at c ^ (r & 7); the per-lane global
-// addresses are permuted so that each wave's contiguous 1 KB LDS write lands in
-// that order.  Rows past M (or N) re-read the last valid row; their results are
-// never stored.
+// Tiled kernel (K % 64 == 0): a BM x BN workgroup tile, BK = 64, WM x WN waves
+// each owning a (BM/WM) x (BN/WN) block of 32x32 MFMA tiles.  Two shapes are
+// built: 128x128 with 4 waves and two workgroups per CU (few active rows), and
+// 256x256 with 8 waves and one workgroup per CU (many rows; half the LDS traffic
+// per flop).  Tiles stream from HBM straight into LDS (buffer_load ... lds, 16
+// bytes per lane) through a ring of stages with one barrier per K-step; every
+// stage is issued (the last one re-issued at the tail) so the wait count is a
+// constant.  In LDS each tile row is eight 16-byte chunks, chunk c of row r at
+// c ^ ((r >> 1) & 7): the 16 lanes that read one MFMA fragment together hit 16
+// different 16-byte bank groups.  Inside a K-step the next k16 fragments are read
+// while the current MFMAs run (one read after each of the first MFMAs).  Rows
+// past M (or N) re-read the last valid row; their results are never stored.
 //
-// Split-K: when the tile count leaves most CUs idle, every tile's K range is cut
-// into S contiguous splits (S chosen on the device from M).  Each split stores
-// its fp32 tile to scratch and bumps the tile's arrival counter; the last split
-// to arrive sums all S partials in split order (deterministic) and runs the
-// epilogue, then resets the counter for the next launch.
+// Split-K (128x128 tiles only, when the tile count leaves CUs idle and K is long):
+// every tile's K range is cut into S contiguous splits.  Each split stores its fp32
+// tile to scratch and bumps the tile's arrival counter; the last split to arrive
+// sums all S partials in split order (deterministic), runs the epilogue and
+// resets the counter for the next launch.
+//
+// Epilogue: each wave moves one 32x32 accumulator block at a time through a
+// private LDS patch and finishes 16 consecutive columns of one row per lane with
+// vector loads and stores.
 //
 // Work units are dealt to the 8 XCDs in contiguous chunks of tile order (a WG
 // runs on XCD blockIdx.x % 8), so the tiles one XCD runs concurrently share A
@@ -68,7 +76,7 @@ FD_DEVICE void epilogue8(const fdh::GemmArgs& g, int row, int col, float v[8]) {
   if constexpr (KIND == fdh::GEMM_QKV || KIND == fdh::GEMM_GELU) {
     if constexpr (KIND == fdh::GEMM_GELU) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] = fd::gelu_tanh(v[e]);
+      for (int e = 0; e < 8; ++e) v[e] = fd::gelu_tanh_fast(v[e]);
     }
     uint4 o;
     o.x = fd::pack_bf2(v[0], v[1]);
@@ -117,8 +125,6 @@ FD_DEVICE void epilogue8(const fdh::GemmArgs& g, int row, int col, float v[8]) {
 
 // ---------------------------------------------------------------- tiled kernel
 
-// Workgroup tile BM x BN, WM x WN waves (each a (BM/WM) x (BN/WN) sub-tile of
-// 32x32 MFMA blocks), STAGES-deep LDS ring, OCC workgroups per CU.
 template <int BM_, int BN_, int WM_, int WN_, int STAGES_, int OCC_>
 struct TileCfg {
   static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, STAGES = STAGES_, OCC = OCC_;
@@ -126,28 +132,17 @@ struct TileCfg {
   static constexpr int TM = BM / WM, TN = BN / WN, FM = TM / 32, FN = TN / 32;
   static constexpr int CHUNKS = (BM + BN) * 8;              // 16-byte chunks per stage
   static constexpr int LOADS = (BM + BN) / 8 / WAVES;       // 8-row wave-loads per wave per stage
-  static_assert((BM + BN) % (8 * WAVES) == 0, "tile rows must split into 8-row wave-loads");
+  static constexpr int LOADS_A = BM / 8 / WAVES;            // the first LOADS_A of them fetch A rows
+  static_assert(BM % (8 * WAVES) == 0 && BN % (8 * WAVES) == 0, "tile rows must split into 8-row wave-loads");
   static_assert(TM % 32 == 0 && TN % 32 == 0, "wave tile must be whole 32x32 MFMA blocks");
+  static_assert(STAGES * CHUNKS * 16 <= 160 * 1024, "ring exceeds LDS");
 };
-
-#ifndef FD_GEMM_CFG
-#define FD_GEMM_CFG 2
-#endif
-#if FD_GEMM_CFG == 0
-using Cfg = TileCfg<256, 128, 2, 2, 3, 1>;
-#elif FD_GEMM_CFG == 1
-using Cfg = TileCfg<256, 128, 4, 2, 3, 1>;
-#elif FD_GEMM_CFG == 2
-using Cfg = TileCfg<128, 128, 2, 2, 2, 2>;
-#else
-using Cfg = TileCfg<256, 256, 2, 4, 2, 1>;
-#endif
+using CfgSmall = TileCfg<128, 128, 2, 2, 2, 2>;
+using CfgLarge = TileCfg<256, 256, 2, 4, 2, 1>;
+constexpr int kSmallTile = 128 * 128;   // split-K partial tile (floats)
 
 constexpr int TBK = 64;
-#ifndef FD_GEMM_MAX_SPLIT
-#define FD_GEMM_MAX_SPLIT 16
-#endif
-constexpr int kMaxSplit = FD_GEMM_MAX_SPLIT;
+constexpr int kMaxSplit = 16;
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 typedef int int32x4_t __attribute__((ext_vector_type(4)));
@@ -180,36 +175,23 @@ FD_DEVICE void wait_vm_barrier() {
   asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" : : "n"(N) : "memory");
 }
 
-FD_DEVICE float split_eff(int units, int cus) {
-  const int waves = (units + cus - 1) / cus;
-  return static_cast<float>(units) / static_cast<float>(waves * cus);
-}
+FD_DEVICE int lds_swizzle(int row) { return (row >> 1) & 7; }
 
-// Number of K splits for `tiles` output tiles and `nk` K-steps (identical in every WG).
+// Number of K splits (identical in every WG): split only while every unit keeps
+// at least 24 K-steps and the units still fit the resident workgroup slots.
 FD_DEVICE int choose_split(int tiles, int nk, int slots, int max_units) {
-  int best = 1;
-  float best_e = split_eff(tiles, slots);
-  for (int s = 2; s <= kMaxSplit; ++s) {
-    if (nk < 4 * s || tiles * s > max_units) break;
-    const float e = split_eff(tiles * s, slots) - 0.05f * static_cast<float>(s - 1);
-    if (e > best_e + 1e-6f) {
-      best_e = e;
-      best = s;
-    }
-  }
-  return best;
+  int s = 1;
+  while (s < kMaxSplit && tiles * (s + 1) <= slots && tiles * (s + 1) <= max_units && nk / (s + 1) >= 24) ++s;
+  return s;
 }
 
-template <int KIND>
+template <class Cfg, int KIND>
 __global__ __launch_bounds__(Cfg::THREADS, Cfg::OCC) void gemm_tiled_kernel(fdh::GemmArgs g, int slots) {
   constexpr int BM = Cfg::BM, BN = Cfg::BN, FM = Cfg::FM, FN = Cfg::FN, TM = Cfg::TM, TN = Cfg::TN;
   constexpr int WAVES = Cfg::WAVES, THREADS = Cfg::THREADS, LOADS = Cfg::LOADS, STAGES = Cfg::STAGES;
-  // the K-loop ring; after the loop it holds the fp32 output tile (row stride OSTRIDE)
-  constexpr int OSTRIDE = BN + 4;
-  constexpr int RING_U4 = STAGES * Cfg::CHUNKS;
-  constexpr int OUT_U4 = BM * OSTRIDE / 4;
-  __shared__ uint4 ring_mem[RING_U4 > OUT_U4 ? RING_U4 : OUT_U4];
-  uint4 (*ring)[Cfg::CHUNKS] = reinterpret_cast<uint4 (*)[Cfg::CHUNKS]>(ring_mem);
+  constexpr int PATCH = 32 * 36;   // per-wave epilogue patch (floats), row stride 36
+  static_assert(WAVES * PATCH * 4 <= STAGES * Cfg::CHUNKS * 16, "epilogue patches must fit in the ring");
+  __shared__ uint4 ring_mem[STAGES * Cfg::CHUNKS];
   __shared__ int s_last;
   const int M = min(*g.m, g.n_max);
   if (M <= 0) return;
@@ -218,20 +200,17 @@ __global__ __launch_bounds__(Cfg::THREADS, Cfg::OCC) void gemm_tiled_kernel(fdh:
   const int tiles_n = (N + BN - 1) / BN;
   const int tiles = tiles_m * tiles_n;
   const int nk = K / TBK;
-  const int S = choose_split(tiles, nk, slots, g.max_units);
+  const int S = (BM * BN == kSmallTile && g.max_units > 0) ? choose_split(tiles, nk, slots, g.max_units) : 1;
   const int units = tiles * S;
   const int per_xcd = (units + kXcds - 1) / kXcds;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / Cfg::WN, wn = wave % Cfg::WN;
   const int l32 = lane & 31, lg = lane >> 5;
-  // this lane's chunk within every 8-row wave-load: row (lane >> 3), logical chunk (lane & 7) ^ (lane >> 3)
-  const int ld_row = lane >> 3;
-  const int ld_chunk = (lane & 7) ^ (lane >> 3);
   const int32x4_t rs_a = buffer_rsrc(g.act);
   const int32x4_t rs_b = buffer_rsrc(g.wt);
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);
-  const uint32_t ring_base = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_ptr_t)&ring[0][0]));
+  const uint32_t ring_base = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_ptr_t)&ring_mem[0]));
 
   for (int u = blockIdx.x; u < per_xcd * kXcds; u += gridDim.x) {
     const int v = (u % kXcds) * per_xcd + u / kXcds;
@@ -240,27 +219,25 @@ __global__ __launch_bounds__(Cfg::THREADS, Cfg::OCC) void gemm_tiled_kernel(fdh:
     const int tm = tile % tiles_m, tn = tile / tiles_m;
     const int m0 = tm * BM, n0 = tn * BN;
     const int kt0 = (split * nk) / S, kt1 = ((split + 1) * nk) / S;
+    const int nkt = kt1 - kt0;
 
-    // per-lane byte offsets of this lane's rows for each of its wave-loads (k = 0)
+    // per-lane byte offsets (k = 0) of this lane's row and source chunk in each of its wave-loads
     uint32_t off[LOADS];
 #pragma unroll
     for (int q = 0; q < LOADS; ++q) {
       const int blk = wave + WAVES * q;        // 8-row block in the concatenated A|B tile
-      const int r = blk * 8 + ld_row;
-      const int gr = (blk * 8 < BM) ? min(m0 + r, M - 1) : min(n0 + (r - BM), N - 1);
-      off[q] = static_cast<uint32_t>((static_cast<size_t>(gr) * K + ld_chunk * 8) * 2);
+      const int r = blk * 8 + (lane >> 3);
+      const int c = (lane & 7) ^ lds_swizzle(r);
+      const int gr = (q < Cfg::LOADS_A) ? min(m0 + r, M - 1) : min(n0 + (r - BM), N - 1);
+      off[q] = static_cast<uint32_t>((static_cast<size_t>(gr) * K + c * 8) * 2);
     }
     auto issue = [&](int kt, int st) {
       const uint32_t buf = ring_base + static_cast<uint32_t>(st * Cfg::CHUNKS * 16);
-      const uint32_t kb = static_cast<uint32_t>(kt * TBK * 2);
+      const uint32_t kb = static_cast<uint32_t>((kt0 + kt) * TBK * 2);
 #pragma unroll
-      for (int q = 0; q < LOADS; ++q) {
-        const uint32_t dst = buf + static_cast<uint32_t>((wave_u + WAVES * q) * 64 * 16);
-        if ((wave + WAVES * q) * 8 < BM)
-          lds_dma16(dst, off[q] + kb, rs_a);
-        else
-          lds_dma16(dst, off[q] + kb, rs_b);
-      }
+      for (int q = 0; q < LOADS; ++q)
+        lds_dma16(buf + static_cast<uint32_t>((wave_u + WAVES * q) * 64 * 16), off[q] + kb,
+                  q < Cfg::LOADS_A ? rs_a : rs_b);
     };
 
     f32x16_t acc[FM][FN];
@@ -271,30 +248,26 @@ __global__ __launch_bounds__(Cfg::THREADS, Cfg::OCC) void gemm_tiled_kernel(fdh:
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-    const int nkt = kt1 - kt0;
 #pragma unroll
-    for (int p = 0; p < STAGES - 1; ++p)
-      if (p < nkt) issue(kt0 + p, p);
+    for (int p = 0; p < STAGES - 1; ++p) issue(min(p, nkt - 1), p);
     for (int it = 0; it < nkt; ++it) {
-      // stage `it` is complete once at most the younger stages' loads are in flight
-      const int younger = min(STAGES - 2, nkt - 1 - it);
-      if (younger >= 2) wait_vm_barrier<2 * LOADS>();
-      else if (younger == 1) wait_vm_barrier<LOADS>();
-      else wait_vm_barrier<0>();
-      if (it + STAGES - 1 < nkt) issue(kt0 + it + STAGES - 1, (it + STAGES - 1) % STAGES);
-      const uint4* sm = ring[it % STAGES];
+      // exactly STAGES - 2 younger stages are in flight: stage `it` has landed for every wave
+      wait_vm_barrier<(STAGES - 2) * LOADS>();
+      // refill the slot every wave finished reading before this barrier (a repeat at the tail)
+      issue(min(it + STAGES - 1, nkt - 1), (it + STAGES - 1) % STAGES);
+      const uint4* sm = ring_mem + (it % STAGES) * Cfg::CHUNKS;
       bf16x8_t a[2][FM], b[2][FN];
       auto frag = [&](int ks, int slot) {
         const int ch = ks * 2 + lg;
 #pragma unroll
         for (int i = 0; i < FM; ++i) {
           const int row = wm * TM + i * 32 + l32;
-          a[slot][i] = __builtin_bit_cast(bf16x8_t, sm[row * 8 + (ch ^ (row & 7))]);
+          a[slot][i] = __builtin_bit_cast(bf16x8_t, sm[row * 8 + (ch ^ lds_swizzle(row))]);
         }
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
           const int row = BM + wn * TN + j * 32 + l32;
-          b[slot][j] = __builtin_bit_cast(bf16x8_t, sm[row * 8 + (ch ^ (row & 7))]);
+          b[slot][j] = __builtin_bit_cast(bf16x8_t, sm[row * 8 + (ch ^ lds_swizzle(row))]);
         }
       };
       frag(0, 0);
@@ -307,8 +280,23 @@ __global__ __launch_bounds__(Cfg::THREADS, Cfg::OCC) void gemm_tiled_kernel(fdh:
           for (int j = 0; j < FN; ++j)
             acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ks & 1][i], b[ks & 1][j], acc[i][j], 0, 0, 0);
       }
+      // schedule: first fragments, then per k16 step one next-step read after each of
+      // the first FM + FN MFMAs, then the remaining MFMAs
+      __builtin_amdgcn_sched_group_barrier(0x100, FM + FN, 0);
+#pragma unroll
+      for (int ks = 0; ks < TBK / 16 - 1; ++ks) {
+#pragma unroll
+        for (int x = 0; x < FM + FN; ++x) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        }
+        __builtin_amdgcn_sched_group_barrier(0x008, FM * FN - (FM + FN), 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, FM * FN, 0);
     }
-    __syncthreads();   // every wave is done with the ring before the next unit refills it
+    // the tail re-issue may still be landing: drain it before the ring is reused
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
 
     if (S > 1) {
       // Store this split's tile (lane-major: element e of thread t at e * THREADS + t)
@@ -356,33 +344,29 @@ __global__ __launch_bounds__(Cfg::THREADS, Cfg::OCC) void gemm_tiled_kernel(fdh:
       }
     }
 
-    // Stage the fp32 tile in LDS (accumulator layout of a 32x32 block: lane holds
-    // column l32, rows 8*(r/4) + 4*lg + (r%4)), then every thread finishes runs
-    // of 8 consecutive columns of a row with vector loads and stores.
-    float* otile = reinterpret_cast<float*>(ring_mem);
+    // Epilogue, one 32x32 block at a time through this wave's LDS patch
+    // (accumulator layout: lane holds column l32, rows 8*(r/4) + 4*lg + (r%4));
+    // lane then owns row lane/2, columns 16*(lane%2) .. +15 of the block.
+    float* patch = reinterpret_cast<float*>(ring_mem) + wave * PATCH;
+    const int pr = lane >> 1, pc = (lane & 1) * 16;
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
-      for (int j = 0; j < FN; ++j)
+      for (int j = 0; j < FN; ++j) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int row = wm * TM + i * 32 + 8 * (r >> 2) + 4 * lg + (r & 3);
-          otile[row * OSTRIDE + wn * TN + j * 32 + l32] = acc[i][j][r];
+        for (int r = 0; r < 16; ++r) patch[(8 * (r >> 2) + 4 * lg + (r & 3)) * 36 + l32] = acc[i][j][r];
+        const int row = m0 + wm * TM + i * 32 + pr, col = n0 + wn * TN + j * 32 + pc;
+        const float4* src = reinterpret_cast<const float4*>(patch + pr * 36 + pc);
+        float v0[8], v1[8];
+        const float4 x0 = src[0], x1 = src[1], x2 = src[2], x3 = src[3];
+        v0[0] = x0.x; v0[1] = x0.y; v0[2] = x0.z; v0[3] = x0.w; v0[4] = x1.x; v0[5] = x1.y; v0[6] = x1.z; v0[7] = x1.w;
+        v1[0] = x2.x; v1[1] = x2.y; v1[2] = x2.z; v1[3] = x2.w; v1[4] = x3.x; v1[5] = x3.y; v1[6] = x3.z; v1[7] = x3.w;
+        if (row < M) {
+          if (col < N) epilogue8<KIND>(g, row, col, v0);
+          if (col + 8 < N) epilogue8<KIND>(g, row, col + 8, v1);
         }
-    __syncthreads();
-    constexpr int RUNS = BM * (BN / 8);
-#pragma unroll 4
-    for (int c = tid; c < RUNS; c += THREADS) {
-      const int lr = c / (BN / 8), lc = (c % (BN / 8)) * 8;
-      const int row = m0 + lr, col = n0 + lc;
-      if (row < M && col < N) {
-        const float4 x0 = *reinterpret_cast<const float4*>(otile + lr * OSTRIDE + lc);
-        const float4 x1 = *reinterpret_cast<const float4*>(otile + lr * OSTRIDE + lc + 4);
-        float v[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
-        epilogue8<KIND>(g, row, col, v);
       }
-    }
-    __syncthreads();   // the tile area is the next unit's ring
+    __syncthreads();   // the patches are the next unit's ring
   }
 }
 
@@ -505,27 +489,42 @@ int gemm_max_tiles() { return 4 * num_cus(); }
 
 size_t gemm_scratch_bytes() {
   const size_t units = static_cast<size_t>(gemm_max_tiles());
-  return units * Cfg::BM * Cfg::BN * sizeof(float) + units * sizeof(int32_t);
+  return units * kSmallTile * sizeof(float) + units * sizeof(int32_t);
 }
+
+namespace {
+// Row capacity (token count of the batch) from which the 256x256 tile is used.
+// The active row count is only known on the device, so the choice rests on the
+// capacity: at the active fractions the gate produces (20-70%), 16384 tokens give
+// thousands of active rows, enough for one 256x256 tile per CU at N >= 1536.
+constexpr int kLargeTileRows = 16384;
+
+template <class Cfg>
+hipError_t launch_tiled(GemmKind kind, const GemmArgs& a, int max_units, hipStream_t s) {
+  const int slots = num_cus() * Cfg::OCC;
+  GemmArgs g = a;
+  g.max_units = max_units;
+  const long long tiles_max =
+      static_cast<long long>((a.n_max + Cfg::BM - 1) / Cfg::BM) * ((a.N + Cfg::BN - 1) / Cfg::BN);
+  long long grid = tiles_max * (max_units > 0 ? kMaxSplit : 1);
+  if (grid > slots) grid = slots;
+  grid = ((grid + kXcds - 1) / kXcds) * kXcds;
+  switch (kind) {
+    case GEMM_QKV: gemm_tiled_kernel<Cfg, GEMM_QKV><<<grid, Cfg::THREADS, 0, s>>>(g, slots); break;
+    case GEMM_RESID: gemm_tiled_kernel<Cfg, GEMM_RESID><<<grid, Cfg::THREADS, 0, s>>>(g, slots); break;
+    case GEMM_GELU: gemm_tiled_kernel<Cfg, GEMM_GELU><<<grid, Cfg::THREADS, 0, s>>>(g, slots); break;
+    case GEMM_EMBED: gemm_tiled_kernel<Cfg, GEMM_EMBED><<<grid, Cfg::THREADS, 0, s>>>(g, slots); break;
+    case GEMM_OUT: gemm_tiled_kernel<Cfg, GEMM_OUT><<<grid, Cfg::THREADS, 0, s>>>(g, slots); break;
+  }
+  return hipGetLastError();
+}
+}  // namespace
 
 hipError_t launch_gemm(GemmKind kind, const GemmArgs& a, hipStream_t s) {
   if (a.K % TBK == 0) {
-    const int slots = num_cus() * Cfg::OCC;
-    GemmArgs g = a;
-    if (!g.partial || !g.counters) g.max_units = 0;   // no scratch: never split
-    const long long tiles_max =
-        static_cast<long long>((a.n_max + Cfg::BM - 1) / Cfg::BM) * ((a.N + Cfg::BN - 1) / Cfg::BN);
-    long long grid = tiles_max * kMaxSplit;
-    if (grid > slots) grid = slots;
-    grid = ((grid + kXcds - 1) / kXcds) * kXcds;
-    switch (kind) {
-      case GEMM_QKV: gemm_tiled_kernel<GEMM_QKV><<<grid, Cfg::THREADS, 0, s>>>(g, slots); break;
-      case GEMM_RESID: gemm_tiled_kernel<GEMM_RESID><<<grid, Cfg::THREADS, 0, s>>>(g, slots); break;
-      case GEMM_GELU: gemm_tiled_kernel<GEMM_GELU><<<grid, Cfg::THREADS, 0, s>>>(g, slots); break;
-      case GEMM_EMBED: gemm_tiled_kernel<GEMM_EMBED><<<grid, Cfg::THREADS, 0, s>>>(g, slots); break;
-      case GEMM_OUT: gemm_tiled_kernel<GEMM_OUT><<<grid, Cfg::THREADS, 0, s>>>(g, slots); break;
-    }
-    return hipGetLastError();
+    const int max_units = (a.partial && a.counters) ? a.max_units : 0;   // no scratch: never split
+    if (a.n_max >= kLargeTileRows && a.N >= 1024) return launch_tiled<CfgLarge>(kind, a, 0, s);
+    return launch_tiled<CfgSmall>(kind, a, max_units, s);
   }
   const long long tiles = static_cast<long long>((a.n_max + BM - 1) / BM) * ((a.N + BN - 1) / BN);
   const long long cap = 2LL * num_cus();

@@ -6,78 +6,96 @@ namespace {
 constexpr int kAdaThreads = 256;
 constexpr int kAdaRowsPerWave = 4;
 constexpr int kAdaRowsPerBlock = kAdaRowsPerWave * (kAdaThreads / fd::kWave);
-constexpr int kAdaMaxB = 8;             // requests handled per pass over a weight row
-constexpr int kAdaLdsFloats = 12288;    // 48 KB of SiLU(cond)
+constexpr int kAdaLdsFloats = 12288;    // at most 48 KB of SiLU(cond) per pass
 
-// mod[b][j] = sum_k W[j][k] * SiLU(cond[b][k]) + bias[j]   (W bf16 [n_out][D]).
-// Each wave owns 4 output rows; lanes stream 16-byte pieces of those rows and
-// dot them with SiLU(cond) staged in LDS for up to 8 requests at a time.
+FD_DEVICE void bf16x8_to_f32(const uint4 w, float f[8]) {
+  const uint32_t r[4] = {w.x, w.y, w.z, w.w};
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    f[2 * q] = __uint_as_float(r[q] << 16);
+    f[2 * q + 1] = __uint_as_float(r[q] & 0xffff0000u);
+  }
+}
+
+// mod[l][b][j] = sum_k W[l][j][k] * SiLU(cond[b][k]) + bias[l][j] for n_blocks
+// stacked weight matrices (W bf16 [n_blocks][n_out][D], rows contiguous across
+// blocks): a stream of n_blocks * n_out weight rows, HBM-bound.  Each wave owns 4
+// consecutive rows; a lane holds 8 consecutive k of each.  KIT = D / 512 fixed
+// (D = 512 KIT): all 4 KIT 16-byte loads of a wave are issued before the first
+// FMA; KIT = 0 is the generic path for other D (one k-chunk of all rows at a
+// time).  SiLU(cond) of NB requests sits in LDS.
+template <int NB, int KIT>
 __global__ __launch_bounds__(kAdaThreads) void adaln_gemv_kernel(const uint16_t* __restrict__ W,
                                                                  const float* __restrict__ bias,
                                                                  const float* __restrict__ cond, int B, int D,
-                                                                 int n_out, int b_chunk, float* __restrict__ mod,
+                                                                 int n_out, int n_rows, float* __restrict__ mod,
                                                                  int32_t* __restrict__ zero_ints, int n_zero) {
-  __shared__ float sc[kAdaLdsFloats];
+  extern __shared__ float sc[];   // [NB][D]
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   // The block's first kernel also clears the GEMM split-K arrival counters.
   if (blockIdx.x == 0 && zero_ints)
     for (int i = threadIdx.x; i < n_zero; i += kAdaThreads) zero_ints[i] = 0;
   const int row0 = blockIdx.x * kAdaRowsPerBlock + wave * kAdaRowsPerWave;
-  for (int b0 = 0; b0 < B; b0 += b_chunk) {
-    const int nb = min(b_chunk, B - b0);
+  const uint16_t* wr[kAdaRowsPerWave];
+#pragma unroll
+  for (int i = 0; i < kAdaRowsPerWave; ++i)
+    wr[i] = W + static_cast<size_t>(min(row0 + i, n_rows - 1)) * D;   // rows past the end re-read the last
+  for (int b0 = 0; b0 < B; b0 += NB) {
     __syncthreads();
-    for (int e = threadIdx.x; e < nb * D; e += kAdaThreads) {
-      const float z = cond[static_cast<size_t>(b0) * D + e];
+    for (int e = threadIdx.x; e < NB * D; e += kAdaThreads) {
+      const int b = b0 + e / D;
+      const float z = b < B ? cond[static_cast<size_t>(b0) * D + e] : 0.f;
       sc[e] = z / (1.0f + __expf(-z));
     }
     __syncthreads();
-    float acc[kAdaRowsPerWave][kAdaMaxB];
+    float acc[kAdaRowsPerWave][NB];
 #pragma unroll
     for (int i = 0; i < kAdaRowsPerWave; ++i)
 #pragma unroll
-      for (int b = 0; b < kAdaMaxB; ++b) acc[i][b] = 0.f;
-    for (int k = lane * 8; k < D; k += fd::kWave * 8) {
-      float s8[kAdaMaxB][8];
+      for (int b = 0; b < NB; ++b) acc[i][b] = 0.f;
+    auto fma_chunk = [&](int k, const uint4* wv) {
 #pragma unroll
-      for (int b = 0; b < kAdaMaxB; ++b) {
-        if (b < nb) {
-          const float4 lo = *reinterpret_cast<const float4*>(&sc[b * D + k]);
-          const float4 hi = *reinterpret_cast<const float4*>(&sc[b * D + k + 4]);
-          s8[b][0] = lo.x; s8[b][1] = lo.y; s8[b][2] = lo.z; s8[b][3] = lo.w;
-          s8[b][4] = hi.x; s8[b][5] = hi.y; s8[b][6] = hi.z; s8[b][7] = hi.w;
+      for (int b = 0; b < NB; ++b) {
+        const float4 lo = *reinterpret_cast<const float4*>(&sc[b * D + k]);
+        const float4 hi = *reinterpret_cast<const float4*>(&sc[b * D + k + 4]);
+        const float s8[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+#pragma unroll
+        for (int i = 0; i < kAdaRowsPerWave; ++i) {
+          float wf[8];
+          bf16x8_to_f32(wv[i], wf);
+          float a = acc[i][b];
+#pragma unroll
+          for (int q = 0; q < 8; ++q) a += wf[q] * s8[q];
+          acc[i][b] = a;
         }
       }
+    };
+    if constexpr (KIT > 0) {
+      uint4 wv[KIT][kAdaRowsPerWave];
 #pragma unroll
-      for (int i = 0; i < kAdaRowsPerWave; ++i) {
-        const int j = row0 + i;
-        if (j >= n_out) break;
-        const uint4 wv = *reinterpret_cast<const uint4*>(W + static_cast<size_t>(j) * D + k);
-        const uint32_t wr[4] = {wv.x, wv.y, wv.z, wv.w};
-        float wf[8];
+      for (int t = 0; t < KIT; ++t)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          wf[2 * q] = __uint_as_float(wr[q] << 16);
-          wf[2 * q + 1] = __uint_as_float(wr[q] & 0xffff0000u);
-        }
+        for (int i = 0; i < kAdaRowsPerWave; ++i)
+          wv[t][i] = *reinterpret_cast<const uint4*>(wr[i] + t * 512 + lane * 8);
 #pragma unroll
-        for (int b = 0; b < kAdaMaxB; ++b) {
-          if (b < nb) {
-            float a = acc[i][b];
+      for (int t = 0; t < KIT; ++t) fma_chunk(t * 512 + lane * 8, wv[t]);
+    } else {
+      for (int k = lane * 8; k < D; k += 512) {
+        uint4 wv[kAdaRowsPerWave];
 #pragma unroll
-            for (int q = 0; q < 8; ++q) a += wf[q] * s8[b][q];
-            acc[i][b] = a;
-          }
-        }
+        for (int i = 0; i < kAdaRowsPerWave; ++i) wv[i] = *reinterpret_cast<const uint4*>(wr[i] + k);
+        fma_chunk(k, wv);
       }
     }
 #pragma unroll
     for (int i = 0; i < kAdaRowsPerWave; ++i) {
       const int j = row0 + i;
 #pragma unroll
-      for (int b = 0; b < kAdaMaxB; ++b) {
-        if (b < nb) {
-          const float s = fd::wave_sum(acc[i][b]);
-          if (lane == 0 && j < n_out) mod[static_cast<size_t>(b0 + b) * n_out + j] = s + bias[j];
+      for (int b = 0; b < NB; ++b) {
+        const float s = fd::wave_sum(acc[i][b]);
+        if (lane == 0 && j < n_rows && b0 + b < B) {
+          const int l = j / n_out, jj = j - l * n_out;
+          mod[(static_cast<size_t>(l) * B + b0 + b) * n_out + jj] = s + bias[j];
         }
       }
     }
@@ -92,7 +110,11 @@ __global__ __launch_bounds__(256) void ln_modulate_kernel(const float* __restric
                                                           const int32_t* __restrict__ cu_q, int B,
                                                           const int32_t* __restrict__ m_dev, int D,
                                                           const float* __restrict__ mod, int mod_stride,
-                                                          int shift_off, int scale_off, uint16_t* __restrict__ a) {
+                                                          int shift_off, int scale_off, uint16_t* __restrict__ a,
+                                                          int32_t* __restrict__ zero_ints, int n_zero) {
+  // optionally the block's first kernel: clear the GEMM / attention arrival counters
+  if (blockIdx.x == 0 && zero_ints)
+    for (int i = threadIdx.x; i < n_zero; i += 256) zero_ints[i] = 0;
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= *m_dev) return;
@@ -146,29 +168,52 @@ __global__ __launch_bounds__(256) void ln_modulate_kernel(const float* __restric
 
 namespace fdh {
 
-hipError_t launch_adaln(const uint16_t* w, const float* b, const float* cond, int B, int D, int n_out, float* mod,
-                        int32_t* zero_ints, int n_zero, hipStream_t s) {
-  int b_chunk = kAdaLdsFloats / D;
-  if (b_chunk > kAdaMaxB) b_chunk = kAdaMaxB;
-  const int grid = (n_out + kAdaRowsPerBlock - 1) / kAdaRowsPerBlock;
-  adaln_gemv_kernel<<<grid, kAdaThreads, 0, s>>>(w, b, cond, B, D, n_out, b_chunk, mod, zero_ints, n_zero);
+hipError_t launch_adaln(const uint16_t* w, const float* b, const float* cond, int B, int D, int n_out, int n_blocks,
+                        float* mod, int32_t* zero_ints, int n_zero, hipStream_t s) {
+  const int n_rows = n_out * n_blocks;
+  const int grid = (n_rows + kAdaRowsPerBlock - 1) / kAdaRowsPerBlock;
+  // requests per pass: B rounded up to a power of two, at most 8 and at most what LDS holds
+  const int cap = kAdaLdsFloats / D;   // >= 1 (D <= 12288)
+  int nb = B <= 1 ? 1 : B <= 2 ? 2 : B <= 4 ? 4 : 8;
+  while (nb > 1 && nb > cap) nb >>= 1;
+  const int kit = (D % 512 == 0 && D <= 2048) ? D / 512 : 0;
+#define FD_ADA(NB, KIT) \
+  adaln_gemv_kernel<NB, KIT><<<grid, kAdaThreads, (NB) * D * sizeof(float), s>>>(w, b, cond, B, D, n_out, n_rows, mod, \
+                                                                                 zero_ints, n_zero)
+#define FD_ADA_NB(NB)                      \
+  switch (kit) {                           \
+    case 1: FD_ADA(NB, 1); break;          \
+    case 2: FD_ADA(NB, 2); break;          \
+    case 3: FD_ADA(NB, 3); break;          \
+    case 4: FD_ADA(NB, 4); break;          \
+    default: FD_ADA(NB, 0);                \
+  }
+  switch (nb) {
+    case 1: FD_ADA_NB(1); break;
+    case 2: FD_ADA_NB(2); break;
+    case 4: FD_ADA_NB(4); break;
+    default: FD_ADA_NB(8);
+  }
+#undef FD_ADA_NB
+#undef FD_ADA
   return hipGetLastError();
 }
 
 hipError_t launch_ln_modulate(const float* h, const int32_t* cu_q, int B, const int32_t* m, int n_max, int D,
                               const float* mod, int mod_stride, int shift_off, int scale_off, uint16_t* a,
-                              hipStream_t s) {
+                              int32_t* zero_ints, int n_zero, hipStream_t s) {
   const int grid = (n_max + 3) / 4;
   switch (D % 256 == 0 ? D / 256 : 0) {
 #define FD_LN_CASE(V)                                                                                   \
   case V:                                                                                               \
-    ln_modulate_kernel<V><<<grid, 256, 0, s>>>(h, cu_q, B, m, D, mod, mod_stride, shift_off, scale_off, a); \
+    ln_modulate_kernel<V><<<grid, 256, 0, s>>>(h, cu_q, B, m, D, mod, mod_stride, shift_off, scale_off, a, zero_ints, n_zero); \
     break;
     FD_LN_CASE(1) FD_LN_CASE(2) FD_LN_CASE(3) FD_LN_CASE(4) FD_LN_CASE(5) FD_LN_CASE(6) FD_LN_CASE(8)
     FD_LN_CASE(12) FD_LN_CASE(16)
 #undef FD_LN_CASE
     default:
-      ln_modulate_kernel<0><<<grid, 256, 0, s>>>(h, cu_q, B, m, D, mod, mod_stride, shift_off, scale_off, a);
+      ln_modulate_kernel<0><<<grid, 256, 0, s>>>(h, cu_q, B, m, D, mod, mod_stride, shift_off, scale_off, a, zero_ints,
+                                                 n_zero);
   }
   return hipGetLastError();
 }

@@ -42,7 +42,7 @@ class FdDims(ctypes.Structure):
 
 class FdBlockWeights(ctypes.Structure):
     _fields_ = [(n, _p) for n in ("w_qkv", "b_qkv", "w_o", "b_o", "w_1", "b_1", "w_2", "b_2",
-                                  "w_ada", "b_ada")]
+                                  "w_ada", "b_ada", "mod")]
 
 
 class FdFinalWeights(ctypes.Structure):
@@ -78,6 +78,7 @@ def lib() -> ctypes.CDLL:
         "fd_select": ([P(FdPlan), _p, _p, FdGate, _p, _p, _p, _p, _p, _p, _p, _p], _i32),
         "fd_gather": ([P(FdPlan), _i32, _p, _p, _p, _p, _p], _i32),
         "fd_embed": ([P(FdPlan), P(FdDims), _p, _p, _p, _p, _p, _p, _p, _p], _i32),
+        "fd_adaln": ([P(FdDims), _i32, _i32, _i32, _p, _p, _p, _p, _p], _i32),
         "fd_block_ws_size": ([P(FdPlan), P(FdDims)], ctypes.c_size_t),
         "fd_block_forward": ([P(FdPlan), P(FdDims), P(FdBlockWeights), _p, _p, _p, _p, _p, _p, _p, _p,
                               ctypes.c_size_t, _p], _i32),
@@ -98,7 +99,7 @@ def lib() -> ctypes.CDLL:
 
 def exported_symbols() -> Sequence[str]:
     return ("fd_last_error", "fd_version", "fd_plan_build", "fd_region_score_ws_size", "fd_region_score",
-            "fd_select", "fd_gather", "fd_embed", "fd_block_ws_size", "fd_block_forward", "fd_final",
+            "fd_select", "fd_gather", "fd_embed", "fd_adaln", "fd_block_ws_size", "fd_block_forward", "fd_final",
             "fd_scatter_update", "fd_timer_arm", "fd_timer_read", "fd_timer_disarm")
 
 
@@ -214,9 +215,15 @@ def fd_block_ws_size(plan: Plan, d: FdDims) -> int:
     return int(lib().fd_block_ws_size(ctypes.byref(plan.c), ctypes.byref(d)))
 
 
-def block_weights(params: Dict[str, torch.Tensor], l: int) -> FdBlockWeights:
+def fd_adaln(d: FdDims, n_blocks: int, n_out: int, n_requests: int, w_ada, b_ada, cond, mod, stream=None) -> None:
+    _check("fd_adaln", lib().fd_adaln(ctypes.byref(d), n_blocks, n_out, n_requests, _ptr(w_ada), _ptr(b_ada),
+                                      _ptr(cond), _ptr(mod), _stream(stream)))
+
+
+def block_weights(params: Dict[str, torch.Tensor], l: int, mod: Optional[torch.Tensor] = None) -> FdBlockWeights:
+    """Weights of block l; `mod` ([B, 6D] fp32, from fd_adaln) replaces the block's own adaLN."""
     names = ("w_qkv", "b_qkv", "w_o", "b_o", "w_1", "b_1", "w_2", "b_2", "w_ada", "b_ada")
-    return FdBlockWeights(*[_ptr(params[n][l]) for n in names])
+    return FdBlockWeights(*[_ptr(params[n][l]) for n in names], _ptr(mod))
 
 
 def final_weights(params: Dict[str, torch.Tensor]) -> FdFinalWeights:
@@ -264,8 +271,9 @@ class SparseStep:
 
     Holds the plan, model parameters (device tensors from workloads.make_params),
     per-block K/V caches, the gate state and the row workspaces; `step()` issues
-    fd_region_score, fd_select, fd_gather, fd_embed, L x fd_block_forward,
-    fd_final and fd_scatter_update on the current stream.
+    fd_region_score, fd_select, fd_gather, fd_embed, fd_adaln (the modulation of
+    all L blocks in one pass), L x fd_block_forward, fd_final and
+    fd_scatter_update on the current stream.
     """
 
     def __init__(self, plan: Plan, d: FdDims, params: Dict[str, torch.Tensor], n_layers: int,
@@ -292,7 +300,8 @@ class SparseStep:
         self.vcache = torch.zeros((N, C), dtype=torch.float32, device=dev)
         self.ws_score = torch.empty(max(fd_region_score_ws_size(plan, C), 256), dtype=torch.uint8, device=dev)
         self.ws_block = torch.empty(fd_block_ws_size(plan, d), dtype=torch.uint8, device=dev)
-        self.block_w = [block_weights(params, l) for l in range(n_layers)]
+        self.mod = torch.zeros((n_layers, B, 6 * D), dtype=torch.float32, device=dev)
+        self.block_w = [block_weights(params, l, self.mod[l]) for l in range(n_layers)]
         self.final_w = final_weights(params)
 
     def reset_gate(self) -> None:
@@ -315,6 +324,8 @@ class SparseStep:
         fd_gather(p, C, x, self.idx, self.m, self.xa, stream)
         fd_embed(p, d, self.xa, self.params["w_e"], self.params["b_e"], self.params["pos"], self.idx, self.m,
                  self.h, stream)
+        fd_adaln(d, self.L, 6 * d.D, p.n_requests, self.params["w_ada"], self.params["b_ada"], cond, self.mod,
+                 stream)
         for l in range(self.L):
             fd_block_forward(p, d, self.block_w[l], cond, self.h, self.idx, self.cu_q, self.m, self.k_cache[l],
                              self.v_cache[l], self.ws_block, stream)

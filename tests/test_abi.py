@@ -110,3 +110,20 @@ def test_block_workspace_size_formula():
     # plus split-K scratch: up to 4 fp32 output tiles (at most 256x256) per CU, and their counters
     cus = 256
     assert rows + 4 * cus * (128 * 128 * 4 + 4) <= got <= rows + 4 * cus * (256 * 256 * 4 + 4) + 8 * 256
+
+
+def test_adaln_validates_before_launch():
+    lib = fdl.lib()
+    d = fdl.FdDims(64, 128, 2, 64, 256)
+    assert lib.fd_adaln(ctypes.byref(d), 2, 768, 1, None, 0x1000, 0x1000, 0x1000, None) == 1
+    assert lib.fd_adaln(ctypes.byref(d), 0, 768, 1, 0x1000, 0x1000, 0x1000, 0x1000, None) == 1
+    assert lib.fd_adaln(ctypes.byref(d), 2, 768, 1, 0x1008, 0x1000, 0x1000, 0x1000, None) == 1
+    bad = fdl.FdDims(64, 96, 2, 64, 256)
+    assert lib.fd_adaln(ctypes.byref(bad), 2, 768, 1, 0x1000, 0x1000, 0x1000, 0x1000, None) == 2
+    # a block with precomputed modulation needs neither cond nor the adaLN weights
+    plan = _fake_plan()
+    w = fdl.FdBlockWeights(*([0x1000] * 8 + [0, 0, 0x1000]))
+    small = (None, 0x1000, 0x1000, 0x1000, 0x1000, 0x1000, 0x1000, 0x1000, 1024, None)
+    assert lib.fd_block_forward(ctypes.byref(plan), ctypes.byref(d), ctypes.byref(w), *small) == 2   # ws too small
+    w0 = fdl.FdBlockWeights(*([0x1000] * 8 + [0, 0, 0]))
+    assert lib.fd_block_forward(ctypes.byref(plan), ctypes.byref(d), ctypes.byref(w0), *small) == 1   # no modulation

@@ -255,3 +255,33 @@ def test_warmup_then_chained_steps_tiny(mode, K):
         x_g, x_o = g["x"], o["x"]
         gate, vc_o = o["gate"], o["vcache"]
         assert rel_err(x_g - x_prev, x_o - x_prev) < gh.TOL
+
+
+def test_block_forward_with_precomputed_modulation_is_identical():
+    """fd_adaln over all blocks at once gives, bit for bit, the modulation a block
+    computes for itself, and it is within fp32-GEMV rounding of the oracle's."""
+    case = gh.make_case("audio", L=2)
+    inp = case.inp
+    g, st = gh.run_gpu(case, inp.eps, inp.x_cur, inp.x_prev)
+    w, p = case.w, case.params_gpu
+    cond = case.cond.cuda()
+    mod = torch.zeros((w.L, w.B, 6 * w.D), dtype=torch.float32, device="cuda")
+    fdl.fd_adaln(case.dims, w.L, 6 * w.D, w.B, p["w_ada"], p["b_ada"], cond, mod)
+    torch.cuda.synchronize()
+    p64 = {k: p[k].cpu().to(torch.float64).numpy() for k in ("w_ada", "b_ada")}
+    for l in range(w.L):
+        ref = np.concatenate(orc.adaln(p64["w_ada"][l], p64["b_ada"][l], case.cond.numpy().astype(np.float64), 6),
+                             axis=-1)
+        assert rel_err(mod[l].cpu().numpy(), ref) < 1e-5
+    h0 = torch.randn((w.N, w.D), generator=torch.Generator().manual_seed(7)).cuda()
+    outs = []
+    for use_mod in (False, True):
+        h = h0.clone()
+        kc, vc = st.k_cache[0].clone(), st.v_cache[0].clone()
+        bw = fdl.block_weights(p, 0, mod[0] if use_mod else None)
+        fdl.fd_block_forward(case.plan, case.dims, bw, None if use_mod else cond, h, st.idx, st.cu_q, st.m, kc, vc,
+                             st.ws_block)
+        torch.cuda.synchronize()
+        outs.append((h.cpu(), kc.cpu(), vc.cpu()))
+    for a, b in zip(*outs):
+        assert torch.equal(a, b)
