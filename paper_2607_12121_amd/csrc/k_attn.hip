@@ -3,17 +3,25 @@
 // ones).  Flash-style with an fp32 online softmax (base-2 exponent); both
 // contractions run on v_mfma_f32_32x32x16_bf16.
 //
-// Work unit = (head, 128-query tile of one request, KV split).  A workgroup of 4
-// waves owns a unit, 32 queries per wave.  Each wave computes S^T = K Q^T (keys x
-// queries), so a lane owns one query column: its running max needs one
-// half-wave exchange per tile and its running sum none until the end; S^T feeds
-// O^T = V^T P^T directly as the B operand.
+// Work unit = (head, query tile of one request, KV split).  A workgroup of 4
+// waves owns a unit; each wave owns 64 queries in two 32-query groups (32 at
+// head dim 128, where two groups would not leave registers for two workgroups
+// per CU).  Each wave
+// computes S^T = K Q^T (keys x queries), so a lane owns one query column: its
+// running max needs one half-wave exchange per tile and its running sum none
+// until the end; S^T feeds O^T = V^T P^T directly as the B operand.  Every K or
+// V fragment read from LDS feeds the MFMAs of both query groups, which halves the
+// LDS read traffic per MFMA (one 1 KB operand per two MFMAs).  Two workgroups
+// share a CU, so one wave's softmax overlaps the other's MFMAs.
 //
 // K and V tiles of 64 keys stream from HBM straight into LDS (buffer_load ...
-// lds) through a ring of stages, both row-major with 16-byte chunk c of key row k
-// stored at c ^ (k % 8).  The V^T operand is read with ds_read_b64_tr_b16: in a
-// group of 16 lanes, lane j addresses 4 consecutive d of key K0 + j/4 and every
-// lane receives its own d for keys K0..K0+3, so V needs no transposing stores.
+// lds) through a ring of stages, both row-major in 16-byte chunks.  K rows are
+// read as MFMA A fragments (16 consecutive keys, one chunk): chunk c of key row
+// k sits at c ^ fk(k).  V^T is read with ds_read_b64_tr_b16: in a group of 16
+// lanes, lane j addresses 4 consecutive d of key K0 + j/4 and every lane
+// receives its own d for keys K0..K0+3, so V needs no transposing stores; one
+// read covers 4 keys x 4 chunks per half-wave, placed at c ^ fv(k).  Both
+// swizzles make every 16-lane (K) or 32-lane (V) read hit distinct banks.
 //
 // When the units of a launch do not fill the CUs, every (head, query tile) is cut
 // into S contiguous key ranges; each split stores its unnormalised O, max and
@@ -21,18 +29,22 @@
 // split order (deterministic).  Units are numbered head-major and dealt to the 8
 // XCDs in contiguous chunks so that the query tiles sharing a head's K/V run on
 // the same L2.
+#include <type_traits>
+
 #include "fd_common.h"
 
 namespace {
 
 constexpr int kXcds = 8;
-constexpr int QB = 128, KB = 64;
+constexpr int KB = 64;                    // keys per tile
 constexpr int kWaves = 4, kThreads = kWaves * 64;
 constexpr int kMaxKvSplit = 16;
+constexpr int kMaxQG = 2;
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 typedef int int32x4_t __attribute__((ext_vector_type(4)));
 typedef short short4_t __attribute__((ext_vector_type(4)));
+using fd::bf16x2_t;
 
 FD_DEVICE int32x4_t buffer_rsrc(const void* base) {
   const uint64_t p = reinterpret_cast<uint64_t>(base);
@@ -57,7 +69,12 @@ FD_DEVICE void wait_vm_barrier() {
 // max / sum of v over lanes l and l ^ 32 (v_permlane32_swap exchanges the halves)
 FD_DEVICE float half_max(float v) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  return __builtin_elementwise_maximum(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+// NaN-propagating maximum (v_maximum3_f32 when nested): unlike fmaxf it needs no
+// canonicalisation of MFMA results
+FD_DEVICE float max3(float a, float b, float c) {
+  return __builtin_elementwise_maximum(__builtin_elementwise_maximum(a, b), c);
 }
 FD_DEVICE float half_sum(float v) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
@@ -66,16 +83,42 @@ FD_DEVICE float half_sum(float v) {
 
 template <int DH>
 struct ACfg {
+  // 32-query groups per wave: two share every K/V fragment read (half the LDS reads
+  // per MFMA); at dh = 128 one, so that two workgroups fit a CU's registers
+  static constexpr int QG = DH >= 128 ? 1 : 2;
+  static constexpr int QB = kWaves * QG * 32;           // queries per unit
   static constexpr int KCH = DH / 8;                    // 16-byte chunks per key row
-  static constexpr int SW = KCH < 8 ? KCH : 8;          // swizzle span
   static constexpr int TILE = KB * KCH;                 // chunks of one K or V tile
   static constexpr int STAGE = 2 * TILE;                // K tile then V tile
-  static constexpr int STAGES = DH >= 128 ? 2 : 3;
+  static constexpr int STAGES = DH >= 128 ? 2 : 3;        // two workgroups per CU fit the LDS
   static constexpr int LOADS = STAGE / 64 / kWaves;     // 1 KB wave-loads per wave per stage
-  static constexpr int KS = DH / 16;                    // k-steps of S^T over d
+  static constexpr int KS = DH / 16;                    // k16 steps of S^T over d
   static constexpr int DT = (DH + 31) / 32;             // 32-row tiles of O^T
+  static constexpr int OCC = 2;                         // workgroups per CU
   static_assert(STAGE % (64 * kWaves) == 0, "stage must split into whole wave-loads");
+  // K: 16 consecutive rows at one chunk -> distinct 16-byte bank groups
+  static constexpr __host__ __device__ int fk(int r) {
+    return KCH >= 16 ? (r & 15) : KCH == 8 ? ((r >> 1) & 7) : ((r >> 3) & (KCH - 1));
+  }
+  // V: 4 consecutive rows x one aligned block of 4 chunks -> distinct bank groups
+  static constexpr __host__ __device__ int fv(int r) { return KCH >= 16 ? 4 * (r & 3) : KCH == 8 ? 4 * ((r >> 1) & 1) : 0; }
+  // the read addressing folds these into per-lane bases plus constants: fk is the
+  // same for key l and l + 32, fv the same for keys k, k + 8 and k + 16 st (k < 8)
+  static constexpr bool swizzle_folds() {
+    for (int r = 0; r < 32; ++r)
+      if (fk(r) != fk(r + 32)) return false;
+    for (int k = 0; k < 8; ++k)
+      for (int st = 0; st < 4; ++st)
+        if (fv(k + 16 * st) != fv(k) || fv(k + 16 * st + 8) != fv(k)) return false;
+    return true;
+  }
+  static_assert(swizzle_folds(), "swizzle must fold into constant offsets");
 };
+
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+FD_DEVICE bf16x8_t lds_read16(uint32_t addr) {
+  return __builtin_bit_cast(bf16x8_t, *(__attribute__((address_space(3))) const u32x4_t*)(uintptr_t)addr);
+}
 
 FD_DEVICE float split_eff(int units, int slots) {
   const int waves = (units + slots - 1) / slots;
@@ -97,13 +140,14 @@ FD_DEVICE int choose_kv_split(int items, int n_kv, int slots, int max_units) {
 }
 
 template <int DH>
-__global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ACfg<DH>::OCC, ACfg<DH>::OCC))) void attn_fwd_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ Kc, const uint16_t* __restrict__ Vc,
     uint16_t* __restrict__ O, int D, int H, const int32_t* __restrict__ cu_q, const int32_t* __restrict__ req_tok_off,
     int B, int max_req_tokens, float scale_log2, float* __restrict__ partial, int32_t* __restrict__ counters,
     int max_units, int slots) {
   using C = ACfg<DH>;
-  __shared__ uint4 ring[C::STAGES][C::STAGE];
+  constexpr int DT = C::DT, KS = C::KS, KCH = C::KCH, STAGES = C::STAGES, LOADS = C::LOADS, QG = C::QG, QB = C::QB;
+  __shared__ uint4 ring[STAGES][C::STAGE];
   __shared__ int s_last;
 
   // query tiles over all requests, then units = heads x tiles x splits
@@ -120,6 +164,24 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
   const int32x4_t rs_k = buffer_rsrc(Kc);
   const int32x4_t rs_v = buffer_rsrc(Vc);
   const uint32_t ring_base = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_ptr_t)&ring[0][0]));
+
+  // V^T operand addressing for ds_read_b64_tr_b16 (see file comment)
+  const int grp = lane >> 4, jj = lane & 15;
+  const int tr_key = 4 * lg + (jj >> 2);                 // + 16 * st + 8 * half
+  const int tr_d = 16 * (grp & 1) + 4 * (jj & 3);       // + 32 * dt
+  const bool tr_live = (DH >= 32) || (grp & 1) == 0;    // rows d >= DH are zero operand rows
+  // per-lane LDS byte offsets inside a tile: K fragment of k16 step ks (key l32), V^T
+  // fragment of 32-row block dt (keys tr_key + 16 st (+ 8)); the swizzles of those keys
+  // do not depend on the half, st or the +8 (checked below)
+  uint32_t k_off[ACfg<DH>::KS], v_off[ACfg<DH>::DT];
+#pragma unroll
+  for (int ks = 0; ks < ACfg<DH>::KS; ++ks)
+    k_off[ks] = static_cast<uint32_t>((l32 * ACfg<DH>::KCH + ((ks * 2 + lg) ^ ACfg<DH>::fk(l32))) * 16);
+#pragma unroll
+  for (int dt = 0; dt < ACfg<DH>::DT; ++dt) {
+    const int d_s = dt * 32 + tr_d;
+    v_off[dt] = static_cast<uint32_t>(tr_key * ACfg<DH>::KCH * 16 + ((d_s >> 3) ^ ACfg<DH>::fv(tr_key)) * 16 + (d_s & 7) * 2);
+  }
 
   for (int u = blockIdx.x; u < per_xcd * kXcds; u += gridDim.x) {
     const int v = (u % kXcds) * per_xcd + u / kXcds;
@@ -141,126 +203,139 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
     const int kt0 = (split * n_kv) / S, kt1 = ((split + 1) * n_kv) / S;
     const int nkt = kt1 - kt0;
     const size_t col0 = static_cast<size_t>(head) * DH;
+    const uint32_t col2 = static_cast<uint32_t>(col0 * 2);
 
-    const int qrow = q_lo + wave * 32 + l32;
-    const bool qvalid = qrow < q_hi;
-    bf16x8_t qf[C::KS];
+    bf16x8_t qf[QG][KS];
 #pragma unroll
-    for (int ks = 0; ks < C::KS; ++ks) {
-      uint4 t = make_uint4(0, 0, 0, 0);
-      if (qvalid) t = *reinterpret_cast<const uint4*>(Q + static_cast<size_t>(qrow) * D + col0 + ks * 16 + lg * 8);
-      qf[ks] = __builtin_bit_cast(bf16x8_t, t);
+    for (int g = 0; g < QG; ++g) {
+      const int qrow = q_lo + wave * (32 * QG) + g * 32 + l32;
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        uint4 t = make_uint4(0, 0, 0, 0);
+        if (qrow < q_hi) t = *reinterpret_cast<const uint4*>(Q + static_cast<size_t>(qrow) * D + col0 + ks * 16 + lg * 8);
+        qf[g][ks] = __builtin_bit_cast(bf16x8_t, t);
+      }
     }
 
-    // this lane's row and source chunk inside each of its wave-loads
+    // DMA of one stage: wave-load q covers 64 consecutive chunks (RPL rows) of the K|V stage
     auto issue = [&](int kt, int st) {
+      constexpr int RPL = 64 / KCH, TILE_BLKS = C::TILE / 64;
       const int k0 = k_beg + kt * KB;
       const uint32_t buf = ring_base + static_cast<uint32_t>(st * C::STAGE * 16);
 #pragma unroll
-      for (int q = 0; q < C::LOADS; ++q) {
-        const int blk = wave + kWaves * q;                 // 1 KB block of the stage
-        const bool is_v = blk * 64 >= C::TILE;
-        const int p = blk * 64 + lane - (is_v ? C::TILE : 0);
-        const int r = p / C::KCH;                          // key row within the tile
-        const int c = (p % C::KCH) ^ (r % C::SW);          // logical chunk
+      for (int q = 0; q < LOADS; ++q) {
+        const int blk = wave_u + kWaves * q;              // wave-uniform
+        const bool is_v = blk >= TILE_BLKS;
+        const int r = (blk - (is_v ? TILE_BLKS : 0)) * RPL + lane / KCH;   // key row within the tile
+        const int c = (lane % KCH) ^ (is_v ? C::fv(r) : C::fk(r));
         const int key = min(k0 + r, k_end - 1);
-        const uint32_t off = static_cast<uint32_t>((static_cast<size_t>(key) * D + col0 + c * 8) * 2);
-        const uint32_t dst = buf + static_cast<uint32_t>((wave_u + kWaves * q) * 64 * 16);
-        if (is_v)
-          lds_dma16(dst, off, rs_v);
-        else
-          lds_dma16(dst, off, rs_k);
+        const uint32_t off = static_cast<uint32_t>(key) * static_cast<uint32_t>(2 * D) + col2 + static_cast<uint32_t>(c * 16);
+        lds_dma16(buf + static_cast<uint32_t>(blk * 64 * 16), off, is_v ? rs_v : rs_k);
       }
     };
 
-    f32x16_t oacc[C::DT];
+    f32x16_t oacc[QG][DT];
 #pragma unroll
-    for (int d = 0; d < C::DT; ++d)
+    for (int g = 0; g < QG; ++g)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) oacc[d][r] = 0.f;
-    float m_run = -INFINITY, l_run = 0.f;
+      for (int d = 0; d < DT; ++d)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) oacc[g][d][r] = 0.f;
+    float m_run[QG], l_run[QG];
+#pragma unroll
+    for (int g = 0; g < QG; ++g) {
+      m_run[g] = -INFINITY;
+      l_run[g] = 0.f;
+    }
 
-    // V^T operand addressing for ds_read_b64_tr_b16 (see file comment)
-    const int grp = lane >> 4, jj = lane & 15;
-    const int tr_key = 4 * lg + (jj >> 2);                 // + 16 * st + 8 * half
-    const int tr_d = 16 * (grp & 1) + 4 * (jj & 3);       // + 32 * dt
-    const bool tr_live = (DH >= 32) || (grp & 1) == 0;    // rows d >= DH are zero operand rows
-
+    // one key tile; MASK: keys past the request end exist in this tile
+    // one key tile; MASK: the tile holds keys past the request end (scores -inf)
+    auto tile = [&](int it, auto mask_tag) {
+      constexpr bool MASK = decltype(mask_tag)::value;
+      const uint32_t kt_addr = ring_base + static_cast<uint32_t>((it % STAGES) * C::STAGE * 16);
+      const uint32_t vt_addr = kt_addr + static_cast<uint32_t>(C::TILE * 16);
+      // S^T (64 keys x 32 queries per group) = K Q^T; each K fragment feeds both groups
+      f32x16_t sacc[QG][2];
+      const f32x16_t zero = {};
 #pragma unroll
-    for (int p = 0; p < C::STAGES - 1; ++p)
-      if (p < nkt) issue(kt0 + p, p);
-    for (int it = 0; it < nkt; ++it) {
-      const int younger = min(C::STAGES - 2, nkt - 1 - it);
-      if (younger >= 1) wait_vm_barrier<C::LOADS>();
-      else wait_vm_barrier<0>();
-      if (it + C::STAGES - 1 < nkt) issue(kt0 + it + C::STAGES - 1, (it + C::STAGES - 1) % C::STAGES);
-      const uint4* kt_lds = ring[it % C::STAGES];
-      const uint32_t vt_addr = ring_base + static_cast<uint32_t>(((it % C::STAGES) * C::STAGE + C::TILE) * 16);
-      const int k0 = k_beg + (kt0 + it) * KB;
-
-      // S^T (64 keys x 32 queries) = K Q^T, two 32-key halves
-      f32x16_t sacc[2];
+      for (int kh = 0; kh < 2; ++kh)
 #pragma unroll
-      for (int kh = 0; kh < 2; ++kh) {
+        for (int ks = 0; ks < KS; ++ks) {
+          // fk(l32 + 32 kh) = fk(l32): the half is a constant offset
+          const uint32_t a_k = kt_addr + k_off[ks] + static_cast<uint32_t>(kh * 32 * KCH * 16);
+          const bf16x8_t a = lds_read16(a_k);
 #pragma unroll
-        for (int r = 0; r < 16; ++r) sacc[kh][r] = 0.f;
-#pragma unroll
-        for (int ks = 0; ks < C::KS; ++ks) {
-          const int key = kh * 32 + l32;
-          const int ch = ks * 2 + lg;
-          const bf16x8_t a = __builtin_bit_cast(bf16x8_t, kt_lds[key * C::KCH + (ch ^ (key % C::SW))]);
-          sacc[kh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[ks], sacc[kh], 0, 0, 0);
+          for (int g = 0; g < QG; ++g)   // the first k16 step starts from the constant zero accumulator
+            sacc[g][kh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[g][ks], ks == 0 ? zero : sacc[g][kh], 0, 0, 0);
         }
+      if constexpr (MASK) {
+        const int lim = k_end - (k_beg + (kt0 + it) * KB) - 4 * lg;   // this lane's keys below lim are valid
+#pragma unroll
+        for (int g = 0; g < QG; ++g)
+#pragma unroll
+          for (int kh = 0; kh < 2; ++kh)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+              if (kh * 32 + 8 * (r >> 2) + (r & 3) >= lim) sacc[g][kh][r] = -INFINITY;
       }
-      // keys past the request end (last tile only): -inf
-      if (k0 + KB > k_end) {
+      // online softmax per group; P packed to bf16 pairs as the B operand of O^T
+      bf16x8_t pk[QG][4];
+#pragma unroll
+      for (int g = 0; g < QG; ++g) {
+        // two independent max3 chains over the 32 scores of this lane
+        float mx0 = __builtin_elementwise_maximum(sacc[g][0][0], sacc[g][0][1]);
+        float mx1 = __builtin_elementwise_maximum(sacc[g][1][0], sacc[g][1][1]);
+#pragma unroll
+        for (int r = 2; r < 16; r += 2) {
+          mx0 = max3(mx0, sacc[g][0][r], sacc[g][0][r + 1]);
+          mx1 = max3(mx1, sacc[g][1][r], sacc[g][1][r + 1]);
+        }
+        const float m_tile = half_max(__builtin_elementwise_maximum(mx0, mx1)) * scale_log2;
+        // Lazy rescaling: the subtracted max only moves when the tile max exceeds it by
+        // more than 8 (P <= 2^8 otherwise); softmax does not depend on that constant.
+        const bool grow = m_tile > m_run[g] + 8.0f;
+        const float m_new = grow ? m_tile : m_run[g];
+        if (__any(grow)) {
+          const float alpha = __builtin_amdgcn_exp2f(m_run[g] - m_new);
+          l_run[g] *= alpha;
+#pragma unroll
+          for (int d = 0; d < DT; ++d)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) oacc[g][d][r] *= alpha;
+        }
+        m_run[g] = m_new;
+        float lsum = 0.f;
 #pragma unroll
         for (int kh = 0; kh < 2; ++kh)
 #pragma unroll
-          for (int r = 0; r < 16; ++r)
-            if (k0 + kh * 32 + 8 * (r >> 2) + 4 * lg + (r & 3) >= k_end) sacc[kh][r] = -INFINITY;
-      }
-      float mx = sacc[0][0];
+          for (int half = 0; half < 2; ++half) {
+            bf16x8_t pv;
 #pragma unroll
-      for (int kh = 0; kh < 2; ++kh)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sacc[kh][r]);
-      const float m_new = fmaxf(m_run, half_max(mx) * scale_log2);
-      if (__any(m_new > m_run)) {   // rescale only when some running max grew
-        const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-        l_run *= alpha;
-#pragma unroll
-        for (int d = 0; d < C::DT; ++d)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) oacc[d][r] *= alpha;
-      }
-      m_run = m_new;
-      bf16x8_t pk[4];
-#pragma unroll
-      for (int kh = 0; kh < 2; ++kh)
-#pragma unroll
-        for (int half = 0; half < 2; ++half) {
-          bf16x8_t pv;
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const float pe = __builtin_amdgcn_exp2f(fmaf(sacc[kh][half * 8 + e], scale_log2, -m_new));
-            l_run += pe;
-            pv[e] = static_cast<__bf16>(pe);
+            for (int e = 0; e < 8; e += 2) {
+              const float p0 = __builtin_amdgcn_exp2f(fmaf(sacc[g][kh][half * 8 + e], scale_log2, -m_new));
+              const float p1 = __builtin_amdgcn_exp2f(fmaf(sacc[g][kh][half * 8 + e + 1], scale_log2, -m_new));
+              const fd::f32x2_t f = {p0, p1};
+              const bf16x2_t pb = __builtin_convertvector(f, bf16x2_t);
+              // the row sum is taken over the rounded P that the PV product uses
+              lsum = __builtin_amdgcn_fdot2_f32_bf16(pb, bf16x2_t{(__bf16)1.0f, (__bf16)1.0f}, lsum, false);
+              pv[e] = pb[0];
+              pv[e + 1] = pb[1];
+            }
+            pk[g][kh * 2 + half] = pv;
           }
-          pk[kh * 2 + half] = pv;
-        }
-      // O^T (d x 32 queries) += V^T P^T; k-step st covers keys 16 st .. 16 st + 15
+        l_run[g] += lsum;
+      }
+      // O^T (d x 32 queries) += V^T P^T; k-step st covers keys 16 st .. 16 st + 15;
+      // each V^T fragment feeds both groups
 #pragma unroll
-      for (int dt = 0; dt < C::DT; ++dt) {
+      for (int dt = 0; dt < DT; ++dt) {
 #pragma unroll
         for (int st = 0; st < 4; ++st) {
           short4_t lo = {0, 0, 0, 0}, hi = {0, 0, 0, 0};
           if (tr_live) {
-            const int d_s = dt * 32 + tr_d;
-            const int key_lo = 16 * st + tr_key, key_hi = key_lo + 8;
-            const int c_lo = (d_s >> 3) ^ (key_lo % C::SW), c_hi = (d_s >> 3) ^ (key_hi % C::SW);
-            const uint32_t a_lo = vt_addr + static_cast<uint32_t>(key_lo * C::KCH * 16 + c_lo * 16 + (d_s & 7) * 2);
-            const uint32_t a_hi = vt_addr + static_cast<uint32_t>(key_hi * C::KCH * 16 + c_hi * 16 + (d_s & 7) * 2);
+            // fv(key) is the same for keys 16 st + tr_key and that + 8: st and hi are constant offsets
+            const uint32_t a_lo = vt_addr + v_off[dt] + static_cast<uint32_t>(16 * st * KCH * 16);
+            const uint32_t a_hi = a_lo + static_cast<uint32_t>(8 * KCH * 16);
             lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) short4_t*)(uintptr_t)a_lo);
             hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) short4_t*)(uintptr_t)a_hi);
           }
@@ -268,24 +343,48 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
           bf16x8_t av;
 #pragma unroll
           for (int e = 0; e < 8; ++e) av[e] = __builtin_bit_cast(__bf16, lo_hi[e]);
-          oacc[dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pk[st], oacc[dt], 0, 0, 0);
+#pragma unroll
+          for (int g = 0; g < QG; ++g) oacc[g][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(av, pk[g][st], oacc[g][dt], 0, 0, 0);
         }
       }
+    };
+
+    // ring: every stage is issued (the last one re-issued at the tail) so the wait count is constant
+#pragma unroll
+    for (int p = 0; p < STAGES - 1; ++p) issue(kt0 + min(p, nkt - 1), p);
+    const bool ragged = (k_beg + kt1 * KB > k_end);   // only the split's last tile can hold keys past the end
+    const int n_plain = ragged ? nkt - 1 : nkt;
+    for (int it = 0; it < n_plain; ++it) {
+      wait_vm_barrier<(STAGES - 2) * LOADS>();
+      issue(kt0 + min(it + STAGES - 1, nkt - 1), (it + STAGES - 1) % STAGES);
+      tile(it, std::integral_constant<bool, false>{});
     }
+    if (ragged) {   // the masked last tile, outside the loop
+      wait_vm_barrier<(STAGES - 2) * LOADS>();
+      issue(kt0 + nkt - 1, (nkt + STAGES - 2) % STAGES);
+      tile(nkt - 1, std::integral_constant<bool, true>{});
+    }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();   // the ring is refilled by the next unit
-    l_run = half_sum(l_run);
+#pragma unroll
+    for (int g = 0; g < QG; ++g) l_run[g] = half_sum(l_run[g]);
 
     if (S > 1) {
       // store this split's unnormalised O, max and sum (lane-major), count the arrival
-      constexpr int E = C::DT * 16 + 2;
+      constexpr int E = QG * (DT * 16 + 2);
       float* slot = partial + static_cast<size_t>(v) * (E * kThreads) + tid;
 #pragma unroll
-      for (int d = 0; d < C::DT; ++d)
+      for (int g = 0; g < QG; ++g) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
-          __hip_atomic_store(slot + (d * 16 + r) * kThreads, oacc[d][r], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(slot + (E - 2) * kThreads, m_run, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      __hip_atomic_store(slot + (E - 1) * kThreads, l_run, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        for (int d = 0; d < DT; ++d)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            __hip_atomic_store(slot + ((g * DT + d) * 16 + r) * kThreads, oacc[g][d][r], __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(slot + (QG * DT * 16 + 2 * g) * kThreads, m_run[g], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(slot + (QG * DT * 16 + 2 * g + 1) * kThreads, l_run[g], __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+      }
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
       __syncthreads();
       if (tid == 0) {
@@ -297,44 +396,52 @@ __global__ __launch_bounds__(kThreads, 2) void attn_fwd_kernel(
       if (!s_last) continue;
       // combine the S splits in split order
       const float* base = partial + static_cast<size_t>(item) * S * (E * kThreads) + tid;
-      float m_all = -INFINITY;
-      for (int s2 = 0; s2 < S; ++s2)
-        m_all = fmaxf(m_all, __hip_atomic_load(base + static_cast<size_t>(s2) * E * kThreads + (E - 2) * kThreads,
-                                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-      float l_all = 0.f;
 #pragma unroll
-      for (int d = 0; d < C::DT; ++d)
+      for (int g = 0; g < QG; ++g) {
+        const int mo = (QG * DT * 16 + 2 * g) * kThreads;
+        float m_all = -INFINITY;
+        for (int s2 = 0; s2 < S; ++s2)
+          m_all = fmaxf(m_all, __hip_atomic_load(base + static_cast<size_t>(s2) * E * kThreads + mo, __ATOMIC_RELAXED,
+                                                 __HIP_MEMORY_SCOPE_AGENT));
+        float l_all = 0.f;
 #pragma unroll
-        for (int r = 0; r < 16; ++r) oacc[d][r] = 0.f;
-      for (int s2 = 0; s2 < S; ++s2) {
-        const float* ps = base + static_cast<size_t>(s2) * E * kThreads;
-        const float ms = __hip_atomic_load(ps + (E - 2) * kThreads, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        const float w = (ms == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(ms - m_all);
-        l_all += w * __hip_atomic_load(ps + (E - 1) * kThreads, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        for (int d = 0; d < DT; ++d)
 #pragma unroll
-        for (int d = 0; d < C::DT; ++d)
+          for (int r = 0; r < 16; ++r) oacc[g][d][r] = 0.f;
+        for (int s2 = 0; s2 < S; ++s2) {
+          const float* ps = base + static_cast<size_t>(s2) * E * kThreads;
+          const float ms = __hip_atomic_load(ps + mo, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          const float w = (ms == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(ms - m_all);
+          l_all += w * __hip_atomic_load(ps + mo + kThreads, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 #pragma unroll
-          for (int r = 0; r < 16; ++r)
-            oacc[d][r] += w * __hip_atomic_load(ps + (d * 16 + r) * kThreads, __ATOMIC_RELAXED,
-                                                __HIP_MEMORY_SCOPE_AGENT);
+          for (int d = 0; d < DT; ++d)
+#pragma unroll
+            for (int r = 0; r < 16; ++r)
+              oacc[g][d][r] += w * __hip_atomic_load(ps + ((g * DT + d) * 16 + r) * kThreads, __ATOMIC_RELAXED,
+                                                     __HIP_MEMORY_SCOPE_AGENT);
+        }
+        l_run[g] = l_all;
       }
-      l_run = l_all;
     }
 
-    if (!qvalid) continue;
-    const float inv_l = 1.0f / l_run;
-    uint16_t* orow = O + static_cast<size_t>(qrow) * D + col0;
 #pragma unroll
-    for (int dt = 0; dt < C::DT; ++dt)
+    for (int g = 0; g < QG; ++g) {
+      const int qrow = q_lo + wave * (32 * QG) + g * 32 + l32;
+      if (qrow >= q_hi) continue;
+      const float inv_l = 1.0f / l_run[g];
+      uint16_t* orow = O + static_cast<size_t>(qrow) * D + col0;
 #pragma unroll
-      for (int r4 = 0; r4 < 4; ++r4) {
-        const int d0 = dt * 32 + 8 * r4 + 4 * lg;
-        if (d0 >= DH) continue;
-        uint2 o;
-        o.x = fd::pack_bf2(oacc[dt][4 * r4 + 0] * inv_l, oacc[dt][4 * r4 + 1] * inv_l);
-        o.y = fd::pack_bf2(oacc[dt][4 * r4 + 2] * inv_l, oacc[dt][4 * r4 + 3] * inv_l);
-        *reinterpret_cast<uint2*>(orow + d0) = o;
-      }
+      for (int dt = 0; dt < DT; ++dt)
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4) {
+          const int d0 = dt * 32 + 8 * r4 + 4 * lg;
+          if (d0 >= DH) continue;
+          uint2 o;
+          o.x = fd::pack_bf2(oacc[g][dt][4 * r4 + 0] * inv_l, oacc[g][dt][4 * r4 + 1] * inv_l);
+          o.y = fd::pack_bf2(oacc[g][dt][4 * r4 + 2] * inv_l, oacc[g][dt][4 * r4 + 3] * inv_l);
+          *reinterpret_cast<uint2*>(orow + d0) = o;
+        }
+    }
   }
 }
 
@@ -344,7 +451,7 @@ namespace fdh {
 
 size_t attn_scratch_bytes(int dh) {
   const size_t units = static_cast<size_t>(gemm_max_tiles());
-  const size_t e = static_cast<size_t>(((dh + 31) / 32) * 16 + 2);
+  const size_t e = static_cast<size_t>(kMaxQG * (((dh + 31) / 32) * 16 + 2));
   return units * e * kThreads * sizeof(float);
 }
 
@@ -354,7 +461,8 @@ hipError_t launch_attention(const uint16_t* q, const uint16_t* kc, const uint16_
   const int slots = 2 * num_cus();
   const int max_units = (partial && counters) ? gemm_max_tiles() : 0;
   // upper bound on the units: every request adds at most one partial query tile
-  const long long items = static_cast<long long>((n_max + QB - 1) / QB + B) * H;
+  const int qb = dh >= 128 ? ACfg<128>::QB : ACfg<64>::QB;
+  const long long items = static_cast<long long>((n_max + qb - 1) / qb + B) * H;
   long long grid = items * kMaxKvSplit;
   if (grid > slots) grid = slots;
   grid = ((grid + kXcds - 1) / kXcds) * kXcds;
