@@ -85,12 +85,15 @@ template <int DH>
 struct ACfg {
   // 32-query groups per wave: two share every K/V fragment read (half the LDS reads
   // per MFMA); at dh = 128 one, so that two workgroups fit a CU's registers
-  static constexpr int QG = DH >= 128 ? 1 : 2;
+  static constexpr int QG = 1;
   static constexpr int QB = kWaves * QG * 32;           // queries per unit
   static constexpr int KCH = DH / 8;                    // 16-byte chunks per key row
   static constexpr int TILE = KB * KCH;                 // chunks of one K or V tile
   static constexpr int STAGE = 2 * TILE;                // K tile then V tile
-  static constexpr int STAGES = DH >= 128 ? 2 : 3;        // two workgroups per CU fit the LDS
+  // dh <= 64: software pipeline (S of tile t + 1 next to the softmax of tile t), four
+  // stages; dh = 128: plain loop, two stages (two workgroups per CU fit the LDS)
+  static constexpr bool PIPE = DH <= 64;
+  static constexpr int STAGES = PIPE ? 4 : 2;
   static constexpr int LOADS = STAGE / 64 / kWaves;     // 1 KB wave-loads per wave per stage
   static constexpr int KS = DH / 16;                    // k16 steps of S^T over d
   static constexpr int DT = (DH + 31) / 32;             // 32-row tiles of O^T
@@ -247,29 +250,32 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ACfg<D
       m_run[g] = -INFINITY;
       l_run[g] = 0.f;
     }
+    typedef f32x16_t SAcc[QG][2];
+    typedef bf16x8_t PAcc[QG][4];
 
-    // one key tile; MASK: keys past the request end exist in this tile
-    // one key tile; MASK: the tile holds keys past the request end (scores -inf)
-    auto tile = [&](int it, auto mask_tag) {
-      constexpr bool MASK = decltype(mask_tag)::value;
-      const uint32_t kt_addr = ring_base + static_cast<uint32_t>((it % STAGES) * C::STAGE * 16);
-      const uint32_t vt_addr = kt_addr + static_cast<uint32_t>(C::TILE * 16);
-      // S^T (64 keys x 32 queries per group) = K Q^T; each K fragment feeds both groups
-      f32x16_t sacc[QG][2];
+    // S^T (64 keys x 32 queries per group) of tile t = K Q^T; each K fragment feeds every group
+    auto s_tile = [&](int t, SAcc& sacc, auto ks_lo_tag, auto ks_hi_tag) {
+      constexpr int KS_LO = decltype(ks_lo_tag)::value, KS_HI = decltype(ks_hi_tag)::value;
+      const uint32_t kt_addr = ring_base + static_cast<uint32_t>((t % STAGES) * C::STAGE * 16);
       const f32x16_t zero = {};
 #pragma unroll
-      for (int kh = 0; kh < 2; ++kh)
+      for (int ks = KS_LO; ks < KS_HI; ++ks)
 #pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
+        for (int kh = 0; kh < 2; ++kh) {
           // fk(l32 + 32 kh) = fk(l32): the half is a constant offset
-          const uint32_t a_k = kt_addr + k_off[ks] + static_cast<uint32_t>(kh * 32 * KCH * 16);
-          const bf16x8_t a = lds_read16(a_k);
+          const bf16x8_t a = lds_read16(kt_addr + k_off[ks] + static_cast<uint32_t>(kh * 32 * KCH * 16));
 #pragma unroll
           for (int g = 0; g < QG; ++g)   // the first k16 step starts from the constant zero accumulator
             sacc[g][kh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[g][ks], ks == 0 ? zero : sacc[g][kh], 0, 0, 0);
         }
+    };
+
+    // Online softmax of tile t, part 1: running max and (rarely) the rescale of O.
+    // MASK: the tile holds keys past the request end (scores -inf).
+    auto softmax_max = [&](int t, SAcc& sacc, float (&m_new)[QG], auto mask_tag) {
+      constexpr bool MASK = decltype(mask_tag)::value;
       if constexpr (MASK) {
-        const int lim = k_end - (k_beg + (kt0 + it) * KB) - 4 * lg;   // this lane's keys below lim are valid
+        const int lim = k_end - (k_beg + (kt0 + t) * KB) - 4 * lg;   // this lane's keys below lim are valid
 #pragma unroll
         for (int g = 0; g < QG; ++g)
 #pragma unroll
@@ -278,8 +284,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ACfg<D
             for (int r = 0; r < 16; ++r)
               if (kh * 32 + 8 * (r >> 2) + (r & 3) >= lim) sacc[g][kh][r] = -INFINITY;
       }
-      // online softmax per group; P packed to bf16 pairs as the B operand of O^T
-      bf16x8_t pk[QG][4];
 #pragma unroll
       for (int g = 0; g < QG; ++g) {
         // two independent max3 chains over the 32 scores of this lane
@@ -294,16 +298,22 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ACfg<D
         // Lazy rescaling: the subtracted max only moves when the tile max exceeds it by
         // more than 8 (P <= 2^8 otherwise); softmax does not depend on that constant.
         const bool grow = m_tile > m_run[g] + 8.0f;
-        const float m_new = grow ? m_tile : m_run[g];
+        m_new[g] = grow ? m_tile : m_run[g];
         if (__any(grow)) {
-          const float alpha = __builtin_amdgcn_exp2f(m_run[g] - m_new);
+          const float alpha = __builtin_amdgcn_exp2f(m_run[g] - m_new[g]);
           l_run[g] *= alpha;
 #pragma unroll
           for (int d = 0; d < DT; ++d)
 #pragma unroll
             for (int r = 0; r < 16; ++r) oacc[g][d][r] *= alpha;
         }
-        m_run[g] = m_new;
+        m_run[g] = m_new[g];
+      }
+    };
+    // part 2: P = exp2(S scale - m) packed to bf16 pairs (the B operand of O^T), row sums
+    auto softmax_p = [&](SAcc& sacc, PAcc& pk, const float (&m_new)[QG]) {
+#pragma unroll
+      for (int g = 0; g < QG; ++g) {
         float lsum = 0.f;
 #pragma unroll
         for (int kh = 0; kh < 2; ++kh)
@@ -312,8 +322,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ACfg<D
             bf16x8_t pv;
 #pragma unroll
             for (int e = 0; e < 8; e += 2) {
-              const float p0 = __builtin_amdgcn_exp2f(fmaf(sacc[g][kh][half * 8 + e], scale_log2, -m_new));
-              const float p1 = __builtin_amdgcn_exp2f(fmaf(sacc[g][kh][half * 8 + e + 1], scale_log2, -m_new));
+              const float p0 = __builtin_amdgcn_exp2f(fmaf(sacc[g][kh][half * 8 + e], scale_log2, -m_new[g]));
+              const float p1 = __builtin_amdgcn_exp2f(fmaf(sacc[g][kh][half * 8 + e + 1], scale_log2, -m_new[g]));
               const fd::f32x2_t f = {p0, p1};
               const bf16x2_t pb = __builtin_convertvector(f, bf16x2_t);
               // the row sum is taken over the rounded P that the PV product uses
@@ -325,12 +335,15 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ACfg<D
           }
         l_run[g] += lsum;
       }
-      // O^T (d x 32 queries) += V^T P^T; k-step st covers keys 16 st .. 16 st + 15;
-      // each V^T fragment feeds both groups
+    };
+
+    // O^T (d x 32 queries) += V^T P^T for tile t; k-step st covers keys 16 st .. 16 st + 15
+    auto pv_tile = [&](int t, PAcc& pk) {
+      const uint32_t vt_addr = ring_base + static_cast<uint32_t>(((t % STAGES) * C::STAGE + C::TILE) * 16);
 #pragma unroll
-      for (int dt = 0; dt < DT; ++dt) {
+      for (int st = 0; st < 4; ++st) {
 #pragma unroll
-        for (int st = 0; st < 4; ++st) {
+        for (int dt = 0; dt < DT; ++dt) {
           short4_t lo = {0, 0, 0, 0}, hi = {0, 0, 0, 0};
           if (tr_live) {
             // fv(key) is the same for keys 16 st + tr_key and that + 8: st and hi are constant offsets
@@ -349,20 +362,141 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ACfg<D
       }
     };
 
-    // ring: every stage is issued (the last one re-issued at the tail) so the wait count is constant
-#pragma unroll
-    for (int p = 0; p < STAGES - 1; ++p) issue(kt0 + min(p, nkt - 1), p);
+    // Software pipeline over the key tiles: iteration t computes S of tile t + 1 on
+    // the MFMA pipe while the VALU runs the softmax of tile t, then O += V P of tile
+    // t.  The ring: stages are issued STAGES - 1 ahead (re-issued at the tail so the
+    // wait count is constant); iteration t refills the slot of tile t - 1, which
+    // every wave finished before the iteration's barrier.
+    constexpr int AHEAD_WAIT = C::PIPE ? (STAGES - 3) * LOADS : 0;   // younger loads allowed while tile t + 1 must have landed
+    SAcc sa, sb;
+    PAcc pk;
+    using I0 = std::integral_constant<int, 0>;
+    using I1 = std::integral_constant<int, 1>;
+    using IK = std::integral_constant<int, KS>;
     const bool ragged = (k_beg + kt1 * KB > k_end);   // only the split's last tile can hold keys past the end
-    const int n_plain = ragged ? nkt - 1 : nkt;
-    for (int it = 0; it < n_plain; ++it) {
+    auto body = [&](int t, SAcc& cur, SAcc& nxt) {
+      wait_vm_barrier<AHEAD_WAIT>();
+      issue(kt0 + min(t + STAGES - 1, nkt - 1), (t + STAGES - 1) % STAGES);
+      float m_new[QG];
+      s_tile(t + 1, nxt, I0{}, I1{});
+      softmax_max(t, cur, m_new, std::integral_constant<bool, false>{});
+      if constexpr (QG == 1) {
+        // Hand-interleaved block: the P math of tile t (16 element pairs) with one or
+        // two MFMA jobs after each pair: first the rest of S(t + 1), then PV(t) per
+        // 16-key step once its P quarter exists.  The order is pinned per chunk.
+        const uint32_t kt_addr = ring_base + static_cast<uint32_t>(((t + 1) % STAGES) * C::STAGE * 16);
+        const uint32_t vt_addr = ring_base + static_cast<uint32_t>(((t % STAGES) * C::STAGE + C::TILE) * 16);
+        constexpr int NS = (KS - 1) * 2, NP = DT * 4, NJ = NS + NP;
+        constexpr int PER = (NJ + 15) / 16;
+        // job j = its LDS operand read (fetch) and its MFMA (run); reads run two jobs ahead
+        auto fetch = [&](int j) -> u32x4_t {
+          if (j < NS) {
+            const int ks = 1 + j / 2, kh = j % 2;
+            return __builtin_bit_cast(u32x4_t, lds_read16(kt_addr + k_off[ks] + static_cast<uint32_t>(kh * 32 * KCH * 16)));
+          }
+          const int st = (j - NS) / DT, dt = (j - NS) % DT;
+          short4_t lo = {0, 0, 0, 0}, hi = {0, 0, 0, 0};
+          if (tr_live) {
+            const uint32_t a_lo = vt_addr + v_off[dt] + static_cast<uint32_t>(16 * st * KCH * 16);
+            const uint32_t a_hi = a_lo + static_cast<uint32_t>(8 * KCH * 16);
+            lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) short4_t*)(uintptr_t)a_lo);
+            hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) short4_t*)(uintptr_t)a_hi);
+          }
+          const short lo_hi[8] = {lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]};
+          return __builtin_bit_cast(u32x4_t, lo_hi);
+        };
+        auto run = [&](int j, u32x4_t op) {
+          const bf16x8_t a = __builtin_bit_cast(bf16x8_t, op);
+          if (j < NS) {
+            const int ks = 1 + j / 2, kh = j % 2;
+            nxt[0][kh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[0][ks], nxt[0][kh], 0, 0, 0);
+          } else {
+            const int st = (j - NS) / DT, dt = (j - NS) % DT;
+            oacc[0][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pk[0][st], oacc[0][dt], 0, 0, 0);
+          }
+        };
+        // earliest pair after which job j may run: S jobs at once, PV(st) after P quarter st
+        auto earliest = [&](int j) { return j < NS ? 0 : 4 * ((j - NS) / DT) + 3; };
+        float lsum = 0.f;
+        int cursor = 0;
+        u32x4_t op0 = fetch(0), op1 = fetch(1);   // operands of jobs cursor and cursor + 1
+        auto next_job = [&]() {
+          const u32x4_t op2 = cursor + 2 < NJ ? fetch(cursor + 2) : op1;
+          run(cursor++, op0);
+          op0 = op1;
+          op1 = op2;
+        };
+#pragma unroll
+        for (int pp = 0; pp < 16; ++pp) {
+          const int kh = pp / 8, half = (pp / 4) % 2, e = 2 * (pp % 4);
+          const float p0 = __builtin_amdgcn_exp2f(fmaf(cur[0][kh][half * 8 + e], scale_log2, -m_new[0]));
+          const float p1 = __builtin_amdgcn_exp2f(fmaf(cur[0][kh][half * 8 + e + 1], scale_log2, -m_new[0]));
+          const fd::f32x2_t f = {p0, p1};
+          const bf16x2_t pb = __builtin_convertvector(f, bf16x2_t);
+          lsum = __builtin_amdgcn_fdot2_f32_bf16(pb, bf16x2_t{(__bf16)1.0f, (__bf16)1.0f}, lsum, false);
+          pk[0][kh * 2 + half][e] = pb[0];
+          pk[0][kh * 2 + half][e + 1] = pb[1];
+#pragma unroll
+          for (int k = 0; k < PER; ++k)
+            if (cursor < NJ && earliest(cursor) <= pp) next_job();
+          __builtin_amdgcn_sched_barrier(0);
+        }
+#pragma unroll
+        for (int k = 0; k < NJ; ++k)
+          if (cursor < NJ) next_job();
+        l_run[0] += lsum;
+      } else {
+        s_tile(t + 1, nxt, I1{}, IK{});
+        softmax_p(cur, pk, m_new);
+        pv_tile(t, pk);
+      }
+    };
+    auto tail = [&](int t, SAcc& cur, bool masked) {
+      float m_new[QG];
+      if (masked)
+        softmax_max(t, cur, m_new, std::integral_constant<bool, true>{});
+      else
+        softmax_max(t, cur, m_new, std::integral_constant<bool, false>{});
+      softmax_p(cur, pk, m_new);
+      pv_tile(t, pk);
+    };
+    if constexpr (C::PIPE) {
+#pragma unroll
+      for (int p = 0; p < STAGES - 1; ++p) issue(kt0 + min(p, nkt - 1), p);
       wait_vm_barrier<(STAGES - 2) * LOADS>();
-      issue(kt0 + min(it + STAGES - 1, nkt - 1), (it + STAGES - 1) % STAGES);
-      tile(it, std::integral_constant<bool, false>{});
-    }
-    if (ragged) {   // the masked last tile, outside the loop
-      wait_vm_barrier<(STAGES - 2) * LOADS>();
-      issue(kt0 + nkt - 1, (nkt + STAGES - 2) % STAGES);
-      tile(nkt - 1, std::integral_constant<bool, true>{});
+      s_tile(0, sa, I0{}, IK{});
+      int t = 0;
+      for (; t + 2 <= nkt - 1; t += 2) {
+        body(t, sa, sb);
+        body(t + 1, sb, sa);
+      }
+      if (t < nkt - 1) {
+        body(t, sa, sb);
+        tail(t + 1, sb, ragged);
+      } else {
+        tail(t, sa, ragged);
+      }
+    } else {
+      // plain loop: the ring is issued STAGES - 1 ahead, tile t is complete after the wait
+      issue(kt0, 0);
+      const int n_plain = ragged ? nkt - 1 : nkt;
+      for (int t = 0; t < n_plain; ++t) {
+        wait_vm_barrier<0>();
+        issue(kt0 + min(t + 1, nkt - 1), (t + 1) % STAGES);
+        s_tile(t, sa, I0{}, IK{});
+        float m_new[QG];
+        softmax_max(t, sa, m_new, std::integral_constant<bool, false>{});
+        softmax_p(sa, pk, m_new);
+        pv_tile(t, pk);
+      }
+      if (ragged) {   // the masked last tile, outside the loop
+        wait_vm_barrier<0>();
+        s_tile(nkt - 1, sa, I0{}, IK{});
+        float m_new[QG];
+        softmax_max(nkt - 1, sa, m_new, std::integral_constant<bool, true>{});
+        softmax_p(sa, pk, m_new);
+        pv_tile(nkt - 1, pk);
+      }
     }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();   // the ring is refilled by the next unit
