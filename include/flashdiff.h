@@ -253,8 +253,10 @@ fd_status fd_scatter_update(const fd_plan* plan, int32_t C, float* x, const floa
 /* ---------------------------------------------------------------- timing
  * Kernel timer for measurement: while armed for `kernel`, every launch of that
  * kernel records a pair of HIP events around it on its stream (up to
- * `capacity` launches).  fd_timer_read synchronises on the recorded events and
- * writes each launch's duration in milliseconds; it returns the count.
+ * `capacity` launches).  The events carry no system-scope memory fence, so
+ * arming the timer does not stall the stream around the timed kernel.
+ * fd_timer_read synchronises on the recorded events and writes each launch's
+ * duration in milliseconds; it returns the count.
  */
 enum {
   FD_K_SCORE = 1, FD_K_SELECT, FD_K_GATHER, FD_K_EMBED, FD_K_ADALN, FD_K_LN,

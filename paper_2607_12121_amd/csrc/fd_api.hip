@@ -395,12 +395,14 @@ fd_status fd_timer_arm(int32_t kernel, int32_t capacity) {
   std::lock_guard<std::mutex> lk(g_timer.mu);
   for (hipEvent_t e : g_timer.ev) (void)hipEventDestroy(e);
   g_timer.ev.assign(2 * static_cast<size_t>(capacity), nullptr);
+  // timing-only events: no system-scope fence (cache write-back and invalidate) at
+  // each record, which would stall the stream between the kernels around it
   for (auto& e : g_timer.ev) {
-    hipError_t r = hipEventCreate(&e);
+    hipError_t r = hipEventCreateWithFlags(&e, hipEventDisableSystemFence);
     if (r != hipSuccess) {
       g_timer.kernel = 0;
       g_timer.capacity = 0;
-      return fdh::hip_fail(r, "hipEventCreate");
+      return fdh::hip_fail(r, "hipEventCreateWithFlags");
     }
   }
   g_timer.kernel = kernel;
