@@ -39,6 +39,7 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--workload", default=WORKLOAD, help="image (default), video, audio, packed or tiny")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU oracle sample")
+    ap.add_argument("--no-hbm", action="store_true", help="skip the streaming-kernel bandwidth figures")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="launch a plain fp32 copy of this many MiB 3 times first (counter calibration)")
     return ap.parse_args()
@@ -58,6 +59,73 @@ def kernel_bytes(name: str, w, M: int) -> float:
     C, N = w.C, w.N
     return {"score": 2.0 * N * C * 4 + 8 * w.R, "gather": M * (C * 4 + C * 2 + 4),
             "scatter": M * (4 * C * 4 + 4)}.get(name, 0.0)
+
+
+def hbm_streams(torch, fdl, wl, pool_bytes: float = 1.1 * 2**30) -> dict:
+    """GB/s of the three streaming kernels (region score, gather, scatter-update)
+    against the 8 TB/s HBM peak, each launch on its own buffers from a pool of more
+    than 1 GiB cycled in order, so the 256 MB MALL cannot serve a launch from the
+    previous ones.  Durations come from the library's event timer around each
+    launch; bytes are the algorithmic ones.  Two figures: the image workload's own
+    shape (one request, ~1-2 MB per launch, bound by launch and ramp latency) and one
+    launch over 64 and over 256 such requests (the packed path scaled up, 40-540 MB
+    per launch)."""
+    shapes = {
+        "image_1_request": wl.WORKLOADS["image"],
+    }
+    for nreq in (64, 256):
+        shapes[f"image_{nreq}_requests"] = wl.Workload(
+            f"image{nreq}", C=64, D=1536, H=24, dh=64, F=6144, L=24,
+            requests=tuple(wl.RequestShape("grid2d", (64, 64), (8, 8)) for _ in range(nreq)),
+            activity="count", activity_args=(26,), dt=-0.02, steps=50, seed=1239)
+    out = {}
+    for label, w in shapes.items():
+        rm = wl.region_map(w)
+        plan = fdl.make_plan(rm.token_region, rm.req_tok_off, rm.n_regions)
+        inp = wl.step_inputs(w, 0, rmap=rm)
+        act = inp.hot
+        tok = np.nonzero(act[rm.token_region])[0].astype(np.int32)
+        M = len(tok)
+        idx = torch.zeros(w.N, dtype=torch.int32, device="cuda")
+        idx[:M] = torch.from_numpy(tok).cuda()
+        m = torch.tensor([M], dtype=torch.int32, device="cuda")
+        active = torch.from_numpy(act.astype(np.uint8)).cuda()
+        dt = torch.from_numpy(wl.dt_per_request(w)).cuda()
+        lat_bytes = w.N * w.C * 4
+        P = max(4, int(np.ceil(pool_bytes / (2 * lat_bytes))))
+        xs = [torch.randn(w.N, w.C, device="cuda") for _ in range(2 * P)]       # P (x_cur, x_prev) pairs
+        vs = [torch.randn(w.N, w.C, device="cuda") for _ in range(P)]           # velocities (first M rows)
+        vcs = [torch.empty(w.N, w.C, device="cuda") for _ in range(P)]          # vcache
+        xa = [torch.empty(w.N, w.C, dtype=torch.int16, device="cuda") for _ in range(P)]
+        score = torch.empty(w.R, dtype=torch.float64, device="cuda")
+        ws = torch.empty(fdl.fd_region_score_ws_size(plan, w.C), dtype=torch.uint8, device="cuda")
+        launches = {
+            "score": lambda i: fdl.fd_region_score(plan, w.C, xs[2 * i], xs[2 * i + 1], score, ws),
+            "gather": lambda i: fdl.fd_gather(plan, w.C, xs[2 * i], idx, m, xa[i]),
+            "scatter": lambda i: fdl.fd_scatter_update(plan, w.C, xs[2 * i + 1], vs[i], idx, m, dt, vcs[i], active,
+                                                       fdl.FD_SKIP_FREEZE),
+        }
+        res = {"tokens": w.N, "requests": w.B, "active_tokens": M, "pool_bytes": 2 * P * lat_bytes, "kernels": {}}
+        for name, fn in launches.items():
+            for i in range(min(P, 4)):
+                fn(i)
+            torch.cuda.synchronize()
+            reps = 2 * P
+            fdl.fd_timer_arm(name, reps)
+            for r in range(reps):
+                fn(r % P)
+            torch.cuda.synchronize()
+            ms = fdl.fd_timer_read(reps)
+            fdl.fd_timer_disarm()
+            avg = float(np.mean(ms))
+            nbytes = kernel_bytes(name, w, M)
+            gbs = nbytes / (avg * 1e-3) / 1e9
+            res["kernels"][name] = {"bytes": nbytes, "avg_us": avg * 1e3, "achieved": gbs, "peak": PEAK_HBM_GBS,
+                                    "unit": "GB/s", "frac": gbs / PEAK_HBM_GBS, "launches": len(ms)}
+        out[label] = res
+        del xs, vs, vcs, xa
+        torch.cuda.empty_cache()
+    return out
 
 
 def step_flops(w, M: int) -> float:
@@ -226,6 +294,9 @@ def main():
                      "launches": len(dom_ms), "avg_ms": dom_avg_ms},
         "kernels_ms_per_step": {k: round(v[0], 4) for k, v in per_kernel.items()},
     }
+    if not args.no_hbm:
+        print("[bench] streaming-kernel bandwidth (score, gather, scatter)", file=sys.stderr, flush=True)
+        out["hbm"] = hbm_streams(torch, fdl, wl)
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
         out["cpu_baseline"] = cpu_baseline(w, params, M, args.cpu_seconds)

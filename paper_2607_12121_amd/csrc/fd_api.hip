@@ -232,7 +232,10 @@ fd_status fd_region_score(const fd_plan* plan, int32_t C, const float* x_cur, co
   FD_REQUIRE(x_cur && x_prev && score && ws, "null pointer");
   FD_REQUIRE(aligned(x_cur, 16) && aligned(x_prev, 16) && aligned(ws, 8), "misaligned buffer");
   if (ws_bytes < fd_region_score_ws_size(plan, C)) return fdh::set_error("score workspace too small"), FD_E_SHAPE;
-  const int rows = score_rows_per_chunk(C);
+  // regions cut into chunks of `rows` tokens, unless there are enough regions to
+  // fill the GPU one workgroup each (then one pass, no finalize)
+  int rows = score_rows_per_chunk(C);
+  if (plan->n_regions >= 2 * fdh::num_cus()) rows = plan->max_region_tokens > 0 ? plan->max_region_tokens : 1;
   const int nchunk = (plan->max_region_tokens + rows - 1) / rows;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   FD_LAUNCH(FD_K_SCORE, s,

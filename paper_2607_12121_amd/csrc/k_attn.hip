@@ -4,15 +4,15 @@
 // contractions run on v_mfma_f32_32x32x16_bf16.
 //
 // Work unit = (head, query tile of one request, KV split).  A workgroup of 4
-// waves owns a unit; each wave owns 64 queries in two 32-query groups (32 at
-// head dim 128, where two groups would not leave registers for two workgroups
-// per CU).  Each wave
-// computes S^T = K Q^T (keys x queries), so a lane owns one query column: its
-// running max needs one half-wave exchange per tile and its running sum none
-// until the end; S^T feeds O^T = V^T P^T directly as the B operand.  Every K or
-// V fragment read from LDS feeds the MFMAs of both query groups, which halves the
-// LDS read traffic per MFMA (one 1 KB operand per two MFMAs).  Two workgroups
-// share a CU, so one wave's softmax overlaps the other's MFMAs.
+// waves owns a unit of 128 queries, 32 per wave (the code also supports two
+// 32-query groups per wave sharing every K/V fragment read; one group measured
+// faster once the loop is software-pipelined).  Each wave computes
+// S^T = K Q^T (keys x queries), so a lane owns one query column: its running max
+// needs one half-wave exchange per tile and its running sum none until the end;
+// S^T feeds O^T = V^T P^T directly as the B operand.  Head dim <= 64 runs a
+// software pipeline (S of the next key tile on the MFMA pipe beside the softmax of
+// the current one); head dim 128 a plain loop.  Two workgroups share a CU, so one
+// wave's softmax overlaps the other's MFMAs.
 //
 // K and V tiles of 64 keys stream from HBM straight into LDS (buffer_load ...
 // lds) through a ring of stages, both row-major in 16-byte chunks.  K rows are
@@ -56,9 +56,12 @@ FD_DEVICE int32x4_t buffer_rsrc(const void* base) {
   return r;
 }
 
-// 16 bytes per lane from buffer offset `voff` into LDS at lds_addr + 16 * lane.
-FD_DEVICE void lds_dma16(uint32_t lds_addr, uint32_t voff, int32x4_t rsrc) {
-  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, 0 offen lds" : : "s"(lds_addr), "v"(voff), "s"(rsrc));
+// 16 bytes per lane from buffer offset voff + soff (soff wave-uniform) into LDS at
+// lds_addr + 16 * lane.
+FD_DEVICE void lds_dma16(uint32_t lds_addr, uint32_t voff, int32x4_t rsrc, uint32_t soff = 0) {
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+               :
+               : "s"(lds_addr), "v"(voff), "s"(rsrc), "s"(soff));
 }
 
 template <int N>
@@ -83,8 +86,8 @@ FD_DEVICE float half_sum(float v) {
 
 template <int DH>
 struct ACfg {
-  // 32-query groups per wave: two share every K/V fragment read (half the LDS reads
-  // per MFMA); at dh = 128 one, so that two workgroups fit a CU's registers
+  // 32-query groups per wave (two would share every K/V fragment read, half the LDS
+  // reads per MFMA, at the cost of the registers the pipeline needs)
   static constexpr int QG = 1;
   static constexpr int QB = kWaves * QG * 32;           // queries per unit
   static constexpr int KCH = DH / 8;                    // 16-byte chunks per key row
@@ -220,20 +223,42 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ACfg<D
       }
     }
 
-    // DMA of one stage: wave-load q covers 64 consecutive chunks (RPL rows) of the K|V stage
-    auto issue = [&](int kt, int st) {
-      constexpr int RPL = 64 / KCH, TILE_BLKS = C::TILE / 64;
-      const int k0 = k_beg + kt * KB;
-      const uint32_t buf = ring_base + static_cast<uint32_t>(st * C::STAGE * 16);
+    // DMA of one stage: wave-load q covers 64 consecutive chunks (RPL rows) of the K|V
+    // stage.  A tile whose keys all lie inside the request adds a wave-uniform byte
+    // offset to per-lane offsets fixed for the unit; only a ragged last tile clamps
+    // its rows per lane.
+    constexpr int RPL = 64 / KCH, TILE_BLKS = C::TILE / 64;
+    const int n_full = (k_end - k_beg) / KB;
+    uint32_t dma_off[LOADS];
 #pragma unroll
-      for (int q = 0; q < LOADS; ++q) {
-        const int blk = wave_u + kWaves * q;              // wave-uniform
-        const bool is_v = blk >= TILE_BLKS;
-        const int r = (blk - (is_v ? TILE_BLKS : 0)) * RPL + lane / KCH;   // key row within the tile
-        const int c = (lane % KCH) ^ (is_v ? C::fv(r) : C::fk(r));
-        const int key = min(k0 + r, k_end - 1);
-        const uint32_t off = static_cast<uint32_t>(key) * static_cast<uint32_t>(2 * D) + col2 + static_cast<uint32_t>(c * 16);
-        lds_dma16(buf + static_cast<uint32_t>(blk * 64 * 16), off, is_v ? rs_v : rs_k);
+    for (int q = 0; q < LOADS; ++q) {
+      const int blk = wave + kWaves * q;
+      const bool is_v = blk >= TILE_BLKS;
+      const int r = (blk - (is_v ? TILE_BLKS : 0)) * RPL + lane / KCH;   // key row within the tile
+      const int c = (lane % KCH) ^ (is_v ? C::fv(r) : C::fk(r));
+      dma_off[q] = static_cast<uint32_t>(k_beg + r) * static_cast<uint32_t>(2 * D) + col2 + static_cast<uint32_t>(c * 16);
+    }
+    auto issue = [&](int kt, int st) {
+      const uint32_t buf = ring_base + static_cast<uint32_t>(st * C::STAGE * 16);
+      if (kt < n_full) {
+        const uint32_t soff = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(kt * KB * 2 * D));
+#pragma unroll
+        for (int q = 0; q < LOADS; ++q) {
+          const int blk = wave_u + kWaves * q;              // wave-uniform
+          lds_dma16(buf + static_cast<uint32_t>(blk * 64 * 16), dma_off[q], blk >= TILE_BLKS ? rs_v : rs_k, soff);
+        }
+      } else {
+        const int k0 = k_beg + kt * KB;
+#pragma unroll
+        for (int q = 0; q < LOADS; ++q) {
+          const int blk = wave_u + kWaves * q;              // wave-uniform
+          const bool is_v = blk >= TILE_BLKS;
+          const int r = (blk - (is_v ? TILE_BLKS : 0)) * RPL + lane / KCH;
+          const int c = (lane % KCH) ^ (is_v ? C::fv(r) : C::fk(r));
+          const int key = min(k0 + r, k_end - 1);
+          const uint32_t off = static_cast<uint32_t>(key) * static_cast<uint32_t>(2 * D) + col2 + static_cast<uint32_t>(c * 16);
+          lds_dma16(buf + static_cast<uint32_t>(blk * 64 * 16), off, is_v ? rs_v : rs_k);
+        }
       }
     };
 

@@ -6,14 +6,18 @@
 namespace {
 
 constexpr int kScoreThreads = 256;
+constexpr int kUnroll = 4;   // independent rows / elements in flight per thread (score)
+constexpr int kStreamUnroll = 8;   // float4 elements in flight per thread (gather, update)
 
 // Partial activity of one chunk of one region: sum of d^2 over `rows_per_chunk`
 // token rows, d = fl32(x_cur - x_prev), accumulated in fp64.  One workgroup per
-// (chunk, region); float4 loads, consecutive lanes on consecutive channels.
+// (chunk, region); float4 loads, consecutive lanes on consecutive channels, each
+// thread's loads for kUnroll elements issued before any is used.  With a single
+// chunk per region the workgroup writes the score itself (no finalize pass).
 __global__ __launch_bounds__(kScoreThreads) void region_score_partial_kernel(
     const int32_t* __restrict__ region_ptr, const int32_t* __restrict__ region_tokens,
     const float* __restrict__ xc, const float* __restrict__ xp, int C, int rows_per_chunk,
-    double* __restrict__ partial) {
+    double* __restrict__ partial, double* __restrict__ score) {
   const int r = blockIdx.y;
   const int nchunk = gridDim.x;
   const int t0 = region_ptr[r], t1 = region_ptr[r + 1];
@@ -22,17 +26,29 @@ __global__ __launch_bounds__(kScoreThreads) void region_score_partial_kernel(
   const int c4 = C >> 2;
   const int n_el = row1 > row0 ? (row1 - row0) * c4 : 0;
   double acc = 0.0;
-  for (int e = threadIdx.x; e < n_el; e += kScoreThreads) {
-    const int row = row0 + e / c4;
-    const int col = e - (e / c4) * c4;
-    const size_t off = static_cast<size_t>(region_tokens[row]) * C;
-    const float4 a = reinterpret_cast<const float4*>(xc + off)[col];
-    const float4 b = reinterpret_cast<const float4*>(xp + off)[col];
-    const double d0 = static_cast<double>(a.x - b.x);
-    const double d1 = static_cast<double>(a.y - b.y);
-    const double d2 = static_cast<double>(a.z - b.z);
-    const double d3 = static_cast<double>(a.w - b.w);
-    acc += (d0 * d0 + d1 * d1) + (d2 * d2 + d3 * d3);
+  for (int e0 = threadIdx.x; e0 < n_el; e0 += kScoreThreads * kUnroll) {
+    float4 a[kUnroll], b[kUnroll];
+#pragma unroll
+    for (int k = 0; k < kUnroll; ++k) {
+      const int e = e0 + k * kScoreThreads;
+      a[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+      b[k] = a[k];
+      if (e < n_el) {
+        const int row = row0 + e / c4;
+        const int col = e - (e / c4) * c4;
+        const size_t off = static_cast<size_t>(region_tokens[row]) * C;
+        a[k] = reinterpret_cast<const float4*>(xc + off)[col];
+        b[k] = reinterpret_cast<const float4*>(xp + off)[col];
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < kUnroll; ++k) {
+      const double d0 = static_cast<double>(a[k].x - b[k].x);
+      const double d1 = static_cast<double>(a[k].y - b[k].y);
+      const double d2 = static_cast<double>(a[k].z - b[k].z);
+      const double d3 = static_cast<double>(a[k].w - b[k].w);
+      acc += (d0 * d0 + d1 * d1) + (d2 * d2 + d3 * d3);
+    }
   }
   acc = fd::wave_sum(acc);
   __shared__ double wsum[kScoreThreads / fd::kWave];
@@ -43,7 +59,10 @@ __global__ __launch_bounds__(kScoreThreads) void region_score_partial_kernel(
     double s = 0.0;
 #pragma unroll
     for (int w = 0; w < kScoreThreads / fd::kWave; ++w) s += wsum[w];
-    partial[static_cast<size_t>(r) * nchunk + blockIdx.x] = s;
+    if (nchunk == 1)
+      score[r] = (0.0 + s) / (static_cast<double>(t1 - t0) * static_cast<double>(C));   // as the finalize pass
+    else
+      partial[static_cast<size_t>(r) * nchunk + blockIdx.x] = s;
   }
 }
 
@@ -150,19 +169,34 @@ __global__ __launch_bounds__(kSelThreads) void gate_select_kernel(
     if (act_s[token_region[u]]) idx[pos++] = u;
 }
 
-// xa[i] = bf16(x[idx[i]]) for i < M; grid-stride over float4 elements.
+// xa[i] = bf16(x[idx[i]]) for i < M.  A workgroup covers kStreamUnroll * 256 consecutive
+// float4 elements of the [M][C/4] grid; pass k of its threads covers 256 of them
+// (whole rows, coalesced), and every thread issues its kStreamUnroll loads (addresses
+// clamped into the grid) before any store, so each wave keeps 8 KB in flight.
 __global__ __launch_bounds__(256) void gather_kernel(const float* __restrict__ x, const int32_t* __restrict__ idx,
                                                      const int32_t* __restrict__ m_dev, int C,
                                                      uint16_t* __restrict__ xa) {
   const int c4 = C >> 2;
   const int total = (*m_dev) * c4;
-  for (int e = blockIdx.x * blockDim.x + threadIdx.x; e < total; e += gridDim.x * blockDim.x) {
+  const int first = blockIdx.x * (256 * kStreamUnroll);
+  if (first >= total) return;
+  float4 v[kStreamUnroll];
+#pragma unroll
+  for (int k = 0; k < kStreamUnroll; ++k) {
+    const int e = min(first + k * 256 + static_cast<int>(threadIdx.x), total - 1);
     const int row = e / c4, col = e - (e / c4) * c4;
-    const float4 v = reinterpret_cast<const float4*>(x + static_cast<size_t>(idx[row]) * C)[col];
-    uint2 o;
-    o.x = fd::pack_bf2(v.x, v.y);
-    o.y = fd::pack_bf2(v.z, v.w);
-    reinterpret_cast<uint2*>(xa + static_cast<size_t>(row) * C)[col] = o;
+    v[k] = reinterpret_cast<const float4*>(x + static_cast<size_t>(idx[row]) * C)[col];
+  }
+#pragma unroll
+  for (int k = 0; k < kStreamUnroll; ++k) {
+    const int e = first + k * 256 + static_cast<int>(threadIdx.x);
+    if (e < total) {
+      const int row = e / c4, col = e - (e / c4) * c4;
+      uint2 o;
+      o.x = fd::pack_bf2(v[k].x, v[k].y);
+      o.y = fd::pack_bf2(v[k].z, v[k].w);
+      reinterpret_cast<uint2*>(xa + static_cast<size_t>(row) * C)[col] = o;
+    }
   }
 }
 
@@ -173,24 +207,53 @@ FD_DEVICE float4 euler4(float4 x, float h, float4 f) {
   return make_float4(x.x + px, x.y + py, x.z + pz, x.w + pw);
 }
 
-// Active rows: x[u] = x[u] + fl32(h_b * v[i]); vcache[u] = v[i], u = idx[i].
+// Active rows: x[u] = x[u] + fl32(h_b * v[i]); vcache[u] = v[i], u = idx[i].  Same
+// decomposition as the gather (kStreamUnroll * 256 elements per workgroup, every
+// load of a thread issued before its stores).
 __global__ __launch_bounds__(256) void update_active_kernel(float* __restrict__ x, const float* __restrict__ v,
                                                             const int32_t* __restrict__ idx,
                                                             const int32_t* __restrict__ m_dev,
                                                             const int32_t* __restrict__ token_region,
                                                             const int32_t* __restrict__ region_req,
-                                                            const float* __restrict__ dt, float* __restrict__ vcache,
-                                                            int C) {
+                                                            const float* __restrict__ dt, int n_req,
+                                                            float* __restrict__ vcache, int C) {
   const int c4 = C >> 2;
   const int total = (*m_dev) * c4;
-  for (int e = blockIdx.x * blockDim.x + threadIdx.x; e < total; e += gridDim.x * blockDim.x) {
+  const int first = blockIdx.x * (256 * kStreamUnroll);
+  if (first >= total) return;
+  // the rows of one workgroup almost always belong to one request: then h is
+  // looked up once (uniform loads), else per row
+  const int last = min(first + 256 * kStreamUnroll, total) - 1;
+  int b_lo = 0, b_hi = 0;
+  if (n_req > 1) {
+    b_lo = region_req[token_region[idx[first / c4]]];
+    b_hi = region_req[token_region[idx[last / c4]]];
+  }
+  const float h_tile = dt[b_lo];
+  int u[kStreamUnroll];
+  float h[kStreamUnroll];
+  float4 f[kStreamUnroll], xv[kStreamUnroll];
+#pragma unroll
+  for (int k = 0; k < kStreamUnroll; ++k) {
+    const int e = min(first + k * 256 + static_cast<int>(threadIdx.x), total - 1);
+    u[k] = idx[e / c4];
+  }
+#pragma unroll
+  for (int k = 0; k < kStreamUnroll; ++k) {
+    const int e = min(first + k * 256 + static_cast<int>(threadIdx.x), total - 1);
     const int row = e / c4, col = e - (e / c4) * c4;
-    const int u = idx[row];
-    const float h = dt[region_req[token_region[u]]];
-    const float4 f = reinterpret_cast<const float4*>(v + static_cast<size_t>(row) * C)[col];
-    float4* xr = reinterpret_cast<float4*>(x + static_cast<size_t>(u) * C) + col;
-    *xr = euler4(*xr, h, f);
-    reinterpret_cast<float4*>(vcache + static_cast<size_t>(u) * C)[col] = f;
+    f[k] = reinterpret_cast<const float4*>(v + static_cast<size_t>(row) * C)[col];
+    xv[k] = reinterpret_cast<const float4*>(x + static_cast<size_t>(u[k]) * C)[col];
+    h[k] = b_lo == b_hi ? h_tile : dt[region_req[token_region[u[k]]]];
+  }
+#pragma unroll
+  for (int k = 0; k < kStreamUnroll; ++k) {
+    const int e = first + k * 256 + static_cast<int>(threadIdx.x);
+    if (e < total) {
+      const int col = e - (e / c4) * c4;
+      reinterpret_cast<float4*>(x + static_cast<size_t>(u[k]) * C)[col] = euler4(xv[k], h[k], f[k]);
+      reinterpret_cast<float4*>(vcache + static_cast<size_t>(u[k]) * C)[col] = f[k];
+    }
   }
 }
 
@@ -219,6 +282,12 @@ int stream_grid(long long elems) {
   return static_cast<int>(g < 1 ? 1 : (g > cap ? cap : g));
 }
 
+// kStreamUnroll elements per thread, grid sized for M = N
+int unrolled_grid(long long elems) {
+  const long long per = 256LL * kStreamUnroll;
+  return static_cast<int>(elems < 1 ? 1 : (elems + per - 1) / per);
+}
+
 }  // namespace
 
 namespace fdh {
@@ -227,9 +296,10 @@ hipError_t launch_region_score(const fd_plan* p, int C, const float* xc, const f
                                double* partial, int nchunk, int rows_per_chunk, hipStream_t s) {
   dim3 grid(nchunk, p->n_regions);
   region_score_partial_kernel<<<grid, kScoreThreads, 0, s>>>(p->region_ptr, p->region_tokens, xc, xp, C,
-                                                             rows_per_chunk, partial);
-  region_score_finalize_kernel<<<(p->n_regions + 255) / 256, 256, 0, s>>>(p->region_ptr, partial, nchunk,
-                                                                          p->n_regions, C, score);
+                                                             rows_per_chunk, partial, score);
+  if (nchunk > 1)
+    region_score_finalize_kernel<<<(p->n_regions + 255) / 256, 256, 0, s>>>(p->region_ptr, partial, nchunk,
+                                                                            p->n_regions, C, score);
   return hipGetLastError();
 }
 
@@ -244,7 +314,7 @@ hipError_t launch_select(const fd_plan* p, const double* score, const double* ep
 
 hipError_t launch_gather(const fd_plan* p, int C, const float* x, const int32_t* idx, const int32_t* m,
                          uint16_t* xa, hipStream_t s) {
-  gather_kernel<<<stream_grid(static_cast<long long>(p->n_tokens) * (C / 4)), 256, 0, s>>>(x, idx, m, C, xa);
+  gather_kernel<<<unrolled_grid(static_cast<long long>(p->n_tokens) * (C / 4)), 256, 0, s>>>(x, idx, m, C, xa);
   return hipGetLastError();
 }
 
@@ -255,8 +325,8 @@ hipError_t launch_scatter_update(const fd_plan* p, int C, float* x, const float*
   if (skip_mode == FD_SKIP_REUSE_DRIFT)
     update_skipped_kernel<<<stream_grid(el), 256, 0, s>>>(x, vcache, active, p->token_region, p->region_req, dt,
                                                          p->n_tokens, C);
-  update_active_kernel<<<stream_grid(el), 256, 0, s>>>(x, v, idx, m, p->token_region, p->region_req, dt, vcache,
-                                                      C);
+  update_active_kernel<<<unrolled_grid(el), 256, 0, s>>>(x, v, idx, m, p->token_region, p->region_req, dt,
+                                                      p->n_requests, vcache, C);
   return hipGetLastError();
 }
 
