@@ -125,6 +125,25 @@ def hbm_streams(torch, fdl, wl, pool_bytes: float = 1.1 * 2**30) -> dict:
         out[label] = res
         del xs, vs, vcs, xa
         torch.cuda.empty_cache()
+    # reference: a plain device copy (torch) of 256 MiB per launch under the same
+    # rotating-buffer rule, read + write bytes
+    n = 64 << 20
+    bufs = [torch.empty(n, device="cuda") for _ in range(10)]
+    outs = [torch.empty(n, device="cuda") for _ in range(10)]
+    outs[0].copy_(bufs[0])
+    ts = []
+    for i in range(10):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        outs[i].copy_(bufs[i])
+        e1.record()
+        torch.cuda.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    t = float(np.median(ts))
+    out["copy_reference"] = {"bytes": 8.0 * n, "avg_us": t * 1e3, "achieved": 8.0 * n / (t * 1e-3) / 1e9,
+                             "unit": "GB/s", "frac": 8.0 * n / (t * 1e-3) / 1e9 / PEAK_HBM_GBS}
+    del bufs, outs
+    torch.cuda.empty_cache()
     return out
 
 

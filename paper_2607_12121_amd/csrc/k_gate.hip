@@ -8,6 +8,7 @@ namespace {
 constexpr int kScoreThreads = 256;
 constexpr int kUnroll = 4;   // independent rows / elements in flight per thread (score)
 constexpr int kStreamUnroll = 8;   // float4 elements in flight per thread (gather, update)
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
 
 // Partial activity of one chunk of one region: sum of d^2 over `rows_per_chunk`
 // token rows, d = fl32(x_cur - x_prev), accumulated in fp64.  One workgroup per
@@ -195,7 +196,9 @@ __global__ __launch_bounds__(256) void gather_kernel(const float* __restrict__ x
       uint2 o;
       o.x = fd::pack_bf2(v[k].x, v[k].y);
       o.y = fd::pack_bf2(v[k].z, v[k].w);
-      reinterpret_cast<uint2*>(xa + static_cast<size_t>(row) * C)[col] = o;
+      // streaming (non-temporal) store: the embedding GEMM reads the rows back once
+      __builtin_nontemporal_store(__builtin_bit_cast(uint64_t, o),
+                                  reinterpret_cast<uint64_t*>(xa + static_cast<size_t>(row) * C) + col);
     }
   }
 }
@@ -251,8 +254,11 @@ __global__ __launch_bounds__(256) void update_active_kernel(float* __restrict__ 
     const int e = first + k * 256 + static_cast<int>(threadIdx.x);
     if (e < total) {
       const int col = e - (e / c4) * c4;
-      reinterpret_cast<float4*>(x + static_cast<size_t>(u[k]) * C)[col] = euler4(xv[k], h[k], f[k]);
-      reinterpret_cast<float4*>(vcache + static_cast<size_t>(u[k]) * C)[col] = f[k];
+      // streaming (non-temporal) stores: neither row is read again within the step
+      __builtin_nontemporal_store(__builtin_bit_cast(f32x4_t, euler4(xv[k], h[k], f[k])),
+                                  reinterpret_cast<f32x4_t*>(x + static_cast<size_t>(u[k]) * C) + col);
+      __builtin_nontemporal_store(__builtin_bit_cast(f32x4_t, f[k]),
+                                  reinterpret_cast<f32x4_t*>(vcache + static_cast<size_t>(u[k]) * C) + col);
     }
   }
 }
