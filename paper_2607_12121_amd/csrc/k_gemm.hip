@@ -138,8 +138,14 @@ struct TileCfg {
   static_assert(STAGES * CHUNKS * 16 <= 160 * 1024, "ring exceeds LDS");
 };
 using CfgSmall = TileCfg<128, 128, 2, 2, 2, 2>;
+using CfgWide = TileCfg<128, 192, 2, 2, 2, 2>;     // 1.5x the columns: one round where 128x128 needs two
+using CfgNarrow = TileCfg<128, 64, 2, 2, 2, 2>;    // half the columns: twice the tiles when few
 using CfgLarge = TileCfg<256, 256, 2, 4, 2, 1>;
 constexpr int kSmallTile = 128 * 128;   // split-K partial tile (floats)
+// LDS ring of the two-workgroups-per-CU kernel: the largest of its three tile shapes
+constexpr int kSmallRing = CfgWide::STAGES * CfgWide::CHUNKS;
+static_assert(kSmallRing >= CfgSmall::STAGES * CfgSmall::CHUNKS + 1 && kSmallRing >= CfgNarrow::STAGES * CfgNarrow::CHUNKS,
+              "the small kernel's ring holds every shape (and the split flag past the 128x128 ring)");
 
 constexpr int TBK = 64;
 constexpr int kMaxSplit = 16;
@@ -185,16 +191,14 @@ FD_DEVICE int choose_split(int tiles, int nk, int slots, int max_units) {
   return s;
 }
 
+// All tiles of one GEMM with tile shape Cfg, the workgroup's LDS ring at ring_mem
+// (STAGES * CHUNKS 16-byte chunks at least) and the split-K arrival flag at s_last.
 template <class Cfg, int KIND>
-__global__ __launch_bounds__(Cfg::THREADS, Cfg::OCC) void gemm_tiled_kernel(fdh::GemmArgs g, int slots) {
+FD_DEVICE void gemm_tiles(const fdh::GemmArgs& g, int slots, int M, uint4* ring_mem, int& s_last) {
   constexpr int BM = Cfg::BM, BN = Cfg::BN, FM = Cfg::FM, FN = Cfg::FN, TM = Cfg::TM, TN = Cfg::TN;
   constexpr int WAVES = Cfg::WAVES, THREADS = Cfg::THREADS, LOADS = Cfg::LOADS, STAGES = Cfg::STAGES;
   constexpr int PATCH = 32 * 36;   // per-wave epilogue patch (floats), row stride 36
   static_assert(WAVES * PATCH * 4 <= STAGES * Cfg::CHUNKS * 16, "epilogue patches must fit in the ring");
-  __shared__ uint4 ring_mem[STAGES * Cfg::CHUNKS];
-  __shared__ int s_last;
-  const int M = min(*g.m, g.n_max);
-  if (M <= 0) return;
   const int N = g.N, K = g.K;
   const int tiles_m = (M + BM - 1) / BM;
   const int tiles_n = (N + BN - 1) / BN;
@@ -370,6 +374,46 @@ __global__ __launch_bounds__(Cfg::THREADS, Cfg::OCC) void gemm_tiled_kernel(fdh:
   }
 }
 
+// Tile shape of the two-workgroups-per-CU kernel for M rows (identical in every
+// WG): 128x128 whenever split-K applies; otherwise the shape whose rounds of tiles
+// over the resident slots cost least, a round of 128x64 / 128x128 / 128x192 tiles
+// weighted 10 / 13 / 22 (measured per-round times at 1664 rows); ties go to the
+// larger tile.  0 = 128x128, 1 = 128x192, 2 = 128x64.
+FD_DEVICE int small_shape(int M, int N, int K, int slots, int max_units) {
+  const int tm = (M + 127) / 128;
+  const int t128 = tm * ((N + 127) / 128);
+  if (max_units > 0 && choose_split(t128, K / TBK, slots, max_units) > 1) return 0;
+  const int r128 = (t128 + slots - 1) / slots;
+  const int r192 = (tm * ((N + 191) / 192) + slots - 1) / slots;
+  const int r64 = (tm * ((N + 63) / 64) + slots - 1) / slots;
+  const int c128 = 13 * r128, c192 = 22 * r192, c64 = 10 * r64;
+  if (c192 <= c128 && c192 <= c64) return 1;
+  if (c128 <= c64) return 0;
+  return 2;
+}
+
+template <int KIND>
+__global__ __launch_bounds__(256, 2) void gemm_small_kernel(fdh::GemmArgs g, int slots) {
+  __shared__ uint4 ring_mem[kSmallRing];
+  int& s_last = *reinterpret_cast<int*>(&ring_mem[kSmallRing - 1]);   // outside the 128x128 ring
+  const int M = min(*g.m, g.n_max);
+  if (M <= 0) return;
+  switch (small_shape(M, g.N, g.K, slots, g.max_units)) {
+    case 1: gemm_tiles<CfgWide, KIND>(g, slots, M, ring_mem, s_last); break;
+    case 2: gemm_tiles<CfgNarrow, KIND>(g, slots, M, ring_mem, s_last); break;
+    default: gemm_tiles<CfgSmall, KIND>(g, slots, M, ring_mem, s_last); break;
+  }
+}
+
+template <int KIND>
+__global__ __launch_bounds__(CfgLarge::THREADS, CfgLarge::OCC) void gemm_large_kernel(fdh::GemmArgs g, int slots) {
+  __shared__ uint4 ring_mem[CfgLarge::STAGES * CfgLarge::CHUNKS];
+  __shared__ int s_last;
+  const int M = min(*g.m, g.n_max);
+  if (M <= 0) return;
+  gemm_tiles<CfgLarge, KIND>(g, slots, M, ring_mem, s_last);
+}
+
 // ---------------------------------------------------------------- simple kernel (any K % 8 == 0)
 
 constexpr int BM = 128, BN = 128, BK = 64;
@@ -499,23 +543,31 @@ namespace {
 // thousands of active rows, enough for one 256x256 tile per CU at N >= 1536.
 constexpr int kLargeTileRows = 16384;
 
-template <class Cfg>
-hipError_t launch_tiled(GemmKind kind, const GemmArgs& a, int max_units, hipStream_t s) {
-  const int slots = num_cus() * Cfg::OCC;
+// Persistent grid: at most the resident slots, at least one workgroup per unit
+// the largest unit count could need (narrowest tile, every split).
+hipError_t launch_tiled(GemmKind kind, const GemmArgs& a, int max_units, bool large, hipStream_t s) {
+  const int occ = large ? CfgLarge::OCC : 2;
+  const int slots = num_cus() * occ;
   GemmArgs g = a;
   g.max_units = max_units;
-  const long long tiles_max =
-      static_cast<long long>((a.n_max + Cfg::BM - 1) / Cfg::BM) * ((a.N + Cfg::BN - 1) / Cfg::BN);
+  const int bm = large ? CfgLarge::BM : 128, bn = large ? CfgLarge::BN : CfgNarrow::BN;
+  const long long tiles_max = static_cast<long long>((a.n_max + bm - 1) / bm) * ((a.N + bn - 1) / bn);
   long long grid = tiles_max * (max_units > 0 ? kMaxSplit : 1);
   if (grid > slots) grid = slots;
   grid = ((grid + kXcds - 1) / kXcds) * kXcds;
+#define FD_GEMM_LAUNCH(K)                                                                      \
+  if (large)                                                                                   \
+    gemm_large_kernel<K><<<grid, CfgLarge::THREADS, 0, s>>>(g, slots);                         \
+  else                                                                                         \
+    gemm_small_kernel<K><<<grid, 256, 0, s>>>(g, slots);
   switch (kind) {
-    case GEMM_QKV: gemm_tiled_kernel<Cfg, GEMM_QKV><<<grid, Cfg::THREADS, 0, s>>>(g, slots); break;
-    case GEMM_RESID: gemm_tiled_kernel<Cfg, GEMM_RESID><<<grid, Cfg::THREADS, 0, s>>>(g, slots); break;
-    case GEMM_GELU: gemm_tiled_kernel<Cfg, GEMM_GELU><<<grid, Cfg::THREADS, 0, s>>>(g, slots); break;
-    case GEMM_EMBED: gemm_tiled_kernel<Cfg, GEMM_EMBED><<<grid, Cfg::THREADS, 0, s>>>(g, slots); break;
-    case GEMM_OUT: gemm_tiled_kernel<Cfg, GEMM_OUT><<<grid, Cfg::THREADS, 0, s>>>(g, slots); break;
+    case GEMM_QKV: FD_GEMM_LAUNCH(GEMM_QKV) break;
+    case GEMM_RESID: FD_GEMM_LAUNCH(GEMM_RESID) break;
+    case GEMM_GELU: FD_GEMM_LAUNCH(GEMM_GELU) break;
+    case GEMM_EMBED: FD_GEMM_LAUNCH(GEMM_EMBED) break;
+    case GEMM_OUT: FD_GEMM_LAUNCH(GEMM_OUT) break;
   }
+#undef FD_GEMM_LAUNCH
   return hipGetLastError();
 }
 }  // namespace
@@ -523,8 +575,8 @@ hipError_t launch_tiled(GemmKind kind, const GemmArgs& a, int max_units, hipStre
 hipError_t launch_gemm(GemmKind kind, const GemmArgs& a, hipStream_t s) {
   if (a.K % TBK == 0) {
     const int max_units = (a.partial && a.counters) ? a.max_units : 0;   // no scratch: never split
-    if (a.n_max >= kLargeTileRows && a.N >= 1024) return launch_tiled<CfgLarge>(kind, a, 0, s);
-    return launch_tiled<CfgSmall>(kind, a, max_units, s);
+    if (a.n_max >= kLargeTileRows && a.N >= 1024) return launch_tiled(kind, a, 0, true, s);
+    return launch_tiled(kind, a, max_units, false, s);
   }
   const long long tiles = static_cast<long long>((a.n_max + BM - 1) / BM) * ((a.N + BN - 1) / BN);
   const long long cap = 2LL * num_cus();
