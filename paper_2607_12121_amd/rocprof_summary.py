@@ -4,8 +4,15 @@
     python -m paper_2607_12121_amd.rocprof_summary traffic --fetch <fetch counter_collection.csv>
         --write <write counter_collection.csv> --kernel REGEX --copy-kernel REGEX
         --copy-bytes S --source FILE [FILE ...] --title T --cmd C [--cmd C ...]
+    python -m paper_2607_12121_amd.rocprof_summary grids <kernel_trace.csv> --title T --cmd C
+        [--include REGEX] [--bytes REGEX@GRID=BYTES ...] [--peak-gbs P]
 
 `stats` turns a `--kernel-trace --stats` kernel table into a markdown table.
+
+`grids` groups a `--kernel-trace` table by kernel and grid size (one line per
+launch shape) with the median, minimum and mean duration; a `--bytes` entry gives
+the algorithmic bytes of the launches of one kernel and grid, from which GB/s
+and the fraction of the peak follow.
 
 `traffic` turns two `--pmc` passes (FETCH_SIZE, then WRITE_SIZE; both in KiB per
 dispatch) into HBM bytes per launch of one kernel.  Each counter is scaled by
@@ -101,6 +108,36 @@ def traffic(a) -> str:
     return "\n".join(out) + "\n"
 
 
+def grids(path: str, title: str, cmds, byte_specs, peak_gbs: float, include=None) -> str:
+    rows = list(csv.DictReader(open(path)))
+    inc = re.compile(include) if include else None
+    dur = defaultdict(list)
+    for r in rows:
+        if inc and not inc.search(_short(r["Kernel_Name"])):
+            continue
+        key = (_short(r["Kernel_Name"]), int(r["Grid_Size_X"]), int(r["Grid_Size_Y"]), int(r["Grid_Size_Z"]))
+        dur[key].append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    nbytes = []
+    for spec in byte_specs or ():
+        rx, rest = spec.rsplit("@", 1)
+        g, b = rest.split("=")
+        nbytes.append((re.compile(rx), int(g), float(b)))
+    out = [f"# {title}", "", "commands (run from the repo root on an MI355X):", ""]
+    out += [f"    {c}" for c in cmds]
+    out += ["", "rocprofv3 kernel durations per launch shape (grid in work-items), microseconds", "",
+            "| kernel | grid | launches | median us | min us | mean us | algorithmic bytes | GB/s (median) | % of peak |",
+            "|---|---|---|---|---|---|---|---|---|"]
+    for key in sorted(dur, key=lambda k: (k[0], k[1] * k[2] * k[3])):
+        v = sorted(dur[key])
+        med = v[len(v) // 2]
+        b = next((nb for rx, g, nb in nbytes if rx.search(key[0]) and g == key[1] * key[2] * key[3]), None)
+        gbs = f"{b / (med * 1e-6) / 1e9:,.0f}" if b else ""
+        frac = f"{b / (med * 1e-6) / 1e9 / peak_gbs * 100:.1f}" if b else ""
+        out.append(f"| {key[0][:60]} | {key[1]}x{key[2]}x{key[3]} | {len(v)} | {med:.2f} | {v[0]:.2f} | "
+                   f"{sum(v) / len(v):.2f} | {f'{b:,.0f}' if b else ''} | {gbs} | {frac} |")
+    return "\n".join(out) + "\n"
+
+
 def read_traffic(path: str, sources):
     """bytes_per_launch from a traffic summary, or None when it is missing or its
     recorded sources differ from `sources` (the kernel changed since the counters)."""
@@ -130,8 +167,20 @@ def main(argv=None):
     t.add_argument("--source", nargs="+", required=True)
     t.add_argument("--title", required=True)
     t.add_argument("--cmd", action="append", required=True)
+    gr = sub.add_parser("grids")
+    gr.add_argument("csv")
+    gr.add_argument("--title", required=True)
+    gr.add_argument("--cmd", action="append", required=True)
+    gr.add_argument("--bytes", action="append")
+    gr.add_argument("--peak-gbs", type=float, default=8000.0)
+    gr.add_argument("--include", help="only kernels whose short name matches this regex")
     a = ap.parse_args(argv)
-    sys.stdout.write(stats(a.csv, a.title, a.cmd) if a.what == "stats" else traffic(a))
+    if a.what == "stats":
+        sys.stdout.write(stats(a.csv, a.title, a.cmd))
+    elif a.what == "grids":
+        sys.stdout.write(grids(a.csv, a.title, a.cmd, a.bytes, a.peak_gbs, a.include))
+    else:
+        sys.stdout.write(traffic(a))
 
 
 if __name__ == "__main__":
