@@ -194,6 +194,23 @@ def test_step_parity_ragged_and_edge_counts():
             assert g["M"] == case.w.N
 
 
+def test_gemm_tile_shapes_with_ragged_columns():
+    """All regions active on a 2560-token, hidden-1024 sequence: 20 row tiles make the
+    MLP up-projection (N = 4096, not a multiple of 192) take the 128x192 tile, the
+    out-projection the 128x64 tile and the down-projection split-K."""
+    w = small_workload("audio", requests=(wl.RequestShape("seq", (2560,), (32,)),), activity="count",
+                       activity_args=(80,), L=1)
+    case = gh.make_case("audio", workload=w)
+    inp = case.inp
+    eps = np.zeros(1)
+    gh.say(f"tile shapes: N={w.N} D={w.D} F={w.F}, all active")
+    g, st = gh.run_gpu(case, eps, inp.x_cur, inp.x_prev)
+    assert g["M"] == w.N
+    rows = np.unique(np.concatenate([[0, w.N - 1], np.random.default_rng(5).choice(w.N, 127, replace=False)]))
+    o = gh.run_oracle(case, eps, inp.x_cur, inp.x_prev, sample_rows=rows)
+    gh.compare_step(case, g, o, inp.x_cur, st)
+
+
 def test_single_region_and_single_token_regions():
     reqs = (wl.RequestShape("grid2d", (8, 8), (8, 8)), wl.RequestShape("grid2d", (4, 12), (1, 1)))
     w = small_workload("tiny", requests=reqs, activity="frac", activity_args=(0.3, 0.6), L=1)
