@@ -4,8 +4,7 @@
 namespace {
 
 constexpr int kAdaThreads = 256;
-constexpr int kAdaRowsPerWave = 4;
-constexpr int kAdaRowsPerBlock = kAdaRowsPerWave * (kAdaThreads / fd::kWave);
+constexpr int kAdaWaves = kAdaThreads / fd::kWave;
 constexpr int kAdaLdsFloats = 12288;    // at most 48 KB of SiLU(cond) per pass
 
 FD_DEVICE void bf16x8_to_f32(const uint4 w, float f[8]) {
@@ -17,14 +16,122 @@ FD_DEVICE void bf16x8_to_f32(const uint4 w, float f[8]) {
   }
 }
 
+// SiLU(cond) of requests b0 .. b0 + NB - 1 (zero past B) into sc[NB][D].
+template <int NB>
+FD_DEVICE void silu_cond_to_lds(const float* __restrict__ cond, int B, int D, int b0, float* sc) {
+  __syncthreads();
+  for (int e = threadIdx.x; e < NB * D; e += kAdaThreads) {
+    const float z = b0 + e / D < B ? cond[static_cast<size_t>(b0) * D + e] : 0.f;
+    sc[e] = z / (1.0f + __expf(-z));
+  }
+  __syncthreads();
+}
+
+// acc[i][b] += dot(W row i (8 bf16 at k, packed in wv[i]), SiLU(cond_b)[k .. k + 7]).
+template <int NB, int R>
+FD_DEVICE void ada_fma_chunk(const float* sc, int D, int k, const uint4 (&wv)[R], float (&acc)[R][NB]) {
+#pragma unroll
+  for (int b = 0; b < NB; ++b) {
+    const float4 lo = *reinterpret_cast<const float4*>(&sc[b * D + k]);
+    const float4 hi = *reinterpret_cast<const float4*>(&sc[b * D + k + 4]);
+    const float s8[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+      float wf[8];
+      bf16x8_to_f32(wv[i], wf);
+      float a = acc[i][b];
+#pragma unroll
+      for (int q = 0; q < 8; ++q) a += wf[q] * s8[q];
+      acc[i][b] = a;
+    }
+  }
+}
+
+// Row j of the stacked weights (block l = j / n_out, output jj): one value per request.
+template <int NB, int R>
+FD_DEVICE void ada_store(const float (&acc)[R][NB], int row0, int n_rows, int n_out, int B, int b0,
+                         const float* __restrict__ bias, float* __restrict__ mod) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int i = 0; i < R; ++i) {
+    const int j = row0 + i;
+#pragma unroll
+    for (int b = 0; b < NB; ++b) {
+      const float s = fd::wave_sum(acc[i][b]);
+      if (lane == 0 && j < n_rows && b0 + b < B) {
+        const int l = j / n_out, jj = j - l * n_out;
+        mod[(static_cast<size_t>(l) * B + b0 + b) * n_out + jj] = s + bias[j];
+      }
+    }
+  }
+}
+
 // mod[l][b][j] = sum_k W[l][j][k] * SiLU(cond[b][k]) + bias[l][j] for n_blocks
 // stacked weight matrices (W bf16 [n_blocks][n_out][D], rows contiguous across
-// blocks): a stream of n_blocks * n_out weight rows, HBM-bound.  Each wave owns 4
-// consecutive rows; a lane holds 8 consecutive k of each.  KIT = D / 512 fixed
-// (D = 512 KIT): all 4 KIT 16-byte loads of a wave are issued before the first
-// FMA; KIT = 0 is the generic path for other D (one k-chunk of all rows at a
-// time).  SiLU(cond) of NB requests sits in LDS.
+// blocks): a stream of n_blocks * n_out weight rows, HBM-bound.  D = 512 KIT: each
+// wave walks groups of 2 consecutive rows (grid-stride), a lane holding 8
+// consecutive k of every 512; two register buffers keep the next group's loads in
+// flight while the current group is reduced.  SiLU(cond) of NB <= 2 requests sits
+// in LDS; B > NB re-streams the weights per NB requests.
 template <int NB, int KIT>
+__global__ __launch_bounds__(kAdaThreads) void adaln_stream_kernel(const uint16_t* __restrict__ W,
+                                                                   const float* __restrict__ bias,
+                                                                   const float* __restrict__ cond, int B, int D,
+                                                                   int n_out, int n_rows, float* __restrict__ mod,
+                                                                   int32_t* __restrict__ zero_ints, int n_zero) {
+  constexpr int R = 2;
+  extern __shared__ float sc[];   // [NB][D]
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  // The block's first kernel also clears the GEMM split-K arrival counters.
+  if (blockIdx.x == 0 && zero_ints)
+    for (int i = threadIdx.x; i < n_zero; i += kAdaThreads) zero_ints[i] = 0;
+  const int n_groups = (n_rows + R - 1) / R;
+  const int stride = gridDim.x * kAdaWaves;
+  auto load = [&](int grp, uint4 (&w)[KIT][R]) {
+#pragma unroll
+    for (int i = 0; i < R; ++i) {
+      const uint16_t* r = W + static_cast<size_t>(min(grp * R + i, n_rows - 1)) * D + lane * 8;   // past the end: the last row again
+#pragma unroll
+      for (int t = 0; t < KIT; ++t) w[t][i] = *reinterpret_cast<const uint4*>(r + t * 512);
+    }
+  };
+  auto reduce = [&](int grp, const uint4 (&w)[KIT][R], int b0) {
+    float acc[R][NB];
+#pragma unroll
+    for (int i = 0; i < R; ++i)
+#pragma unroll
+      for (int b = 0; b < NB; ++b) acc[i][b] = 0.f;
+#pragma unroll
+    for (int t = 0; t < KIT; ++t) ada_fma_chunk<NB, R>(sc, D, t * 512 + lane * 8, w[t], acc);
+    ada_store<NB, R>(acc, grp * R, n_rows, n_out, B, b0, bias, mod);
+  };
+  for (int b0 = 0; b0 < B; b0 += NB) {
+    silu_cond_to_lds<NB>(cond, B, D, b0, sc);
+    int grp = blockIdx.x * kAdaWaves + wave;
+    if (grp >= n_groups) continue;
+    uint4 w0[KIT][R], w1[KIT][R];
+    load(grp, w0);
+    for (;;) {
+      const bool more0 = grp + stride < n_groups;
+      if (more0) load(grp + stride, w1);
+      reduce(grp, w0, b0);
+      if (!more0) break;
+      grp += stride;
+      const bool more1 = grp + stride < n_groups;
+      if (more1) load(grp + stride, w0);
+      reduce(grp, w1, b0);
+      if (!more1) break;
+      grp += stride;
+    }
+  }
+}
+
+// The same product for any D (and for more than two requests per pass, where the
+// streaming kernel's registers would grow past two waves per SIMD): one group of 4
+// rows per wave, one k-chunk of all 4 rows at a time.
+constexpr int kAdaRowsPerWave = 4;
+constexpr int kAdaRowsPerBlock = kAdaRowsPerWave * kAdaWaves;
+template <int NB>
 __global__ __launch_bounds__(kAdaThreads) void adaln_gemv_kernel(const uint16_t* __restrict__ W,
                                                                  const float* __restrict__ bias,
                                                                  const float* __restrict__ cond, int B, int D,
@@ -32,7 +139,6 @@ __global__ __launch_bounds__(kAdaThreads) void adaln_gemv_kernel(const uint16_t*
                                                                  int32_t* __restrict__ zero_ints, int n_zero) {
   extern __shared__ float sc[];   // [NB][D]
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  // The block's first kernel also clears the GEMM split-K arrival counters.
   if (blockIdx.x == 0 && zero_ints)
     for (int i = threadIdx.x; i < n_zero; i += kAdaThreads) zero_ints[i] = 0;
   const int row0 = blockIdx.x * kAdaRowsPerBlock + wave * kAdaRowsPerWave;
@@ -41,64 +147,19 @@ __global__ __launch_bounds__(kAdaThreads) void adaln_gemv_kernel(const uint16_t*
   for (int i = 0; i < kAdaRowsPerWave; ++i)
     wr[i] = W + static_cast<size_t>(min(row0 + i, n_rows - 1)) * D;   // rows past the end re-read the last
   for (int b0 = 0; b0 < B; b0 += NB) {
-    __syncthreads();
-    for (int e = threadIdx.x; e < NB * D; e += kAdaThreads) {
-      const int b = b0 + e / D;
-      const float z = b < B ? cond[static_cast<size_t>(b0) * D + e] : 0.f;
-      sc[e] = z / (1.0f + __expf(-z));
-    }
-    __syncthreads();
+    silu_cond_to_lds<NB>(cond, B, D, b0, sc);
     float acc[kAdaRowsPerWave][NB];
 #pragma unroll
     for (int i = 0; i < kAdaRowsPerWave; ++i)
 #pragma unroll
       for (int b = 0; b < NB; ++b) acc[i][b] = 0.f;
-    auto fma_chunk = [&](int k, const uint4* wv) {
+    for (int k = lane * 8; k < D; k += 512) {
+      uint4 wv[kAdaRowsPerWave];
 #pragma unroll
-      for (int b = 0; b < NB; ++b) {
-        const float4 lo = *reinterpret_cast<const float4*>(&sc[b * D + k]);
-        const float4 hi = *reinterpret_cast<const float4*>(&sc[b * D + k + 4]);
-        const float s8[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
-#pragma unroll
-        for (int i = 0; i < kAdaRowsPerWave; ++i) {
-          float wf[8];
-          bf16x8_to_f32(wv[i], wf);
-          float a = acc[i][b];
-#pragma unroll
-          for (int q = 0; q < 8; ++q) a += wf[q] * s8[q];
-          acc[i][b] = a;
-        }
-      }
-    };
-    if constexpr (KIT > 0) {
-      uint4 wv[KIT][kAdaRowsPerWave];
-#pragma unroll
-      for (int t = 0; t < KIT; ++t)
-#pragma unroll
-        for (int i = 0; i < kAdaRowsPerWave; ++i)
-          wv[t][i] = *reinterpret_cast<const uint4*>(wr[i] + t * 512 + lane * 8);
-#pragma unroll
-      for (int t = 0; t < KIT; ++t) fma_chunk(t * 512 + lane * 8, wv[t]);
-    } else {
-      for (int k = lane * 8; k < D; k += 512) {
-        uint4 wv[kAdaRowsPerWave];
-#pragma unroll
-        for (int i = 0; i < kAdaRowsPerWave; ++i) wv[i] = *reinterpret_cast<const uint4*>(wr[i] + k);
-        fma_chunk(k, wv);
-      }
+      for (int i = 0; i < kAdaRowsPerWave; ++i) wv[i] = *reinterpret_cast<const uint4*>(wr[i] + k);
+      ada_fma_chunk<NB, kAdaRowsPerWave>(sc, D, k, wv, acc);
     }
-#pragma unroll
-    for (int i = 0; i < kAdaRowsPerWave; ++i) {
-      const int j = row0 + i;
-#pragma unroll
-      for (int b = 0; b < NB; ++b) {
-        const float s = fd::wave_sum(acc[i][b]);
-        if (lane == 0 && j < n_rows && b0 + b < B) {
-          const int l = j / n_out, jj = j - l * n_out;
-          mod[(static_cast<size_t>(l) * B + b0 + b) * n_out + jj] = s + bias[j];
-        }
-      }
-    }
+    ada_store<NB, kAdaRowsPerWave>(acc, row0, n_rows, n_out, B, b0, bias, mod);
   }
 }
 
@@ -171,31 +232,45 @@ namespace fdh {
 hipError_t launch_adaln(const uint16_t* w, const float* b, const float* cond, int B, int D, int n_out, int n_blocks,
                         float* mod, int32_t* zero_ints, int n_zero, hipStream_t s) {
   const int n_rows = n_out * n_blocks;
-  const int grid = (n_rows + kAdaRowsPerBlock - 1) / kAdaRowsPerBlock;
   // requests per pass: B rounded up to a power of two, at most 8 and at most what LDS holds
   const int cap = kAdaLdsFloats / D;   // >= 1 (D <= 12288)
   int nb = B <= 1 ? 1 : B <= 2 ? 2 : B <= 4 ? 4 : 8;
   while (nb > 1 && nb > cap) nb >>= 1;
   const int kit = (D % 512 == 0 && D <= 2048) ? D / 512 : 0;
-#define FD_ADA(NB, KIT) \
-  adaln_gemv_kernel<NB, KIT><<<grid, kAdaThreads, (NB) * D * sizeof(float), s>>>(w, b, cond, B, D, n_out, n_rows, mod, \
-                                                                                 zero_ints, n_zero)
-#define FD_ADA_NB(NB)                      \
-  switch (kit) {                           \
-    case 1: FD_ADA(NB, 1); break;          \
-    case 2: FD_ADA(NB, 2); break;          \
-    case 3: FD_ADA(NB, 3); break;          \
-    case 4: FD_ADA(NB, 4); break;          \
-    default: FD_ADA(NB, 0);                \
+  if (kit > 0 && nb <= 2) {
+    // persistent: four workgroups per CU, fewer when the rows run out first
+    const int groups = (n_rows + 1) / 2;
+    int grid = 4 * num_cus();
+    if (grid > (groups + kAdaWaves - 1) / kAdaWaves) grid = (groups + kAdaWaves - 1) / kAdaWaves;
+#define FD_ADA(NB, KIT)                                                                                     \
+  adaln_stream_kernel<NB, KIT><<<grid, kAdaThreads, (NB) * D * sizeof(float), s>>>(w, b, cond, B, D, n_out, \
+                                                                                 n_rows, mod, zero_ints, n_zero)
+#define FD_ADA_NB(NB)             \
+  switch (kit) {                  \
+    case 1: FD_ADA(NB, 1); break; \
+    case 2: FD_ADA(NB, 2); break; \
+    case 3: FD_ADA(NB, 3); break; \
+    default: FD_ADA(NB, 4);       \
   }
-  switch (nb) {
-    case 1: FD_ADA_NB(1); break;
-    case 2: FD_ADA_NB(2); break;
-    case 4: FD_ADA_NB(4); break;
-    default: FD_ADA_NB(8);
-  }
+    if (nb == 1) {
+      FD_ADA_NB(1)
+    } else {
+      FD_ADA_NB(2)
+    }
 #undef FD_ADA_NB
 #undef FD_ADA
+  } else {
+    const int grid = (n_rows + kAdaRowsPerBlock - 1) / kAdaRowsPerBlock;
+#define FD_ADA(NB) \
+  adaln_gemv_kernel<NB><<<grid, kAdaThreads, (NB) * D * sizeof(float), s>>>(w, b, cond, B, D, n_out, n_rows, mod, zero_ints, n_zero)
+    switch (nb) {
+      case 1: FD_ADA(1); break;
+      case 2: FD_ADA(2); break;
+      case 4: FD_ADA(4); break;
+      default: FD_ADA(8);
+    }
+#undef FD_ADA
+  }
   return hipGetLastError();
 }
 
