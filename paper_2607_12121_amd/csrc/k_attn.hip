@@ -23,12 +23,14 @@
 // read covers 4 keys x 4 chunks per half-wave, placed at c ^ fv(k).  Both
 // swizzles make every 16-lane (K) or 32-lane (V) read hit distinct banks.
 //
-// When the units of a launch do not fill the CUs, every (head, query tile) is cut
-// into S contiguous key ranges; each split stores its unnormalised O, max and
-// sum with device-coherent stores and the last split to arrive combines them in
-// split order (deterministic).  Units are numbered head-major and dealt to the 8
-// XCDs in contiguous chunks so that the query tiles sharing a head's K/V run on
-// the same L2.
+// Schedule: the key tiles of all (head, query tile) items, head-major, form one
+// range cut into equal contiguous shares, one per workgroup of the persistent grid;
+// a share that ends inside an item leaves a piece of it to the next share.  Each
+// piece of a cut item stores its unnormalised O, max and sum with device-coherent
+// stores and the last piece to arrive combines them in key order (deterministic
+// for a given grid).  Shares are dealt to the 8 XCDs in contiguous chunks so that
+// the query tiles sharing a head's K/V run on the same L2.  Without scratch for a
+// partial per piece the shares are runs of whole items.
 #include <type_traits>
 
 #include "fd_common.h"
@@ -38,7 +40,6 @@ namespace {
 constexpr int kXcds = 8;
 constexpr int KB = 64;                    // keys per tile
 constexpr int kWaves = 4, kThreads = kWaves * 64;
-constexpr int kMaxKvSplit = 16;
 constexpr int kMaxQG = 2;
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
@@ -126,43 +127,31 @@ FD_DEVICE bf16x8_t lds_read16(uint32_t addr) {
   return __builtin_bit_cast(bf16x8_t, *(__attribute__((address_space(3))) const u32x4_t*)(uintptr_t)addr);
 }
 
-FD_DEVICE float split_eff(int units, int slots) {
-  const int waves = (units + slots - 1) / slots;
-  return static_cast<float>(units) / static_cast<float>(waves * slots);
-}
-
-FD_DEVICE int choose_kv_split(int items, int n_kv, int slots, int max_units) {
-  int best = 1;
-  float best_e = split_eff(items, slots);
-  for (int s = 2; s <= kMaxKvSplit; ++s) {
-    if (n_kv < 4 * s || items * s > max_units) break;
-    const float e = split_eff(items * s, slots) - 0.03f * static_cast<float>(s - 1);
-    if (e > best_e + 1e-6f) {
-      best_e = e;
-      best = s;
-    }
-  }
-  return best;
-}
-
 template <int DH>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ACfg<DH>::OCC, ACfg<DH>::OCC))) void attn_fwd_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ Kc, const uint16_t* __restrict__ Vc,
     uint16_t* __restrict__ O, int D, int H, const int32_t* __restrict__ cu_q, const int32_t* __restrict__ req_tok_off,
-    int B, int max_req_tokens, float scale_log2, float* __restrict__ partial, int32_t* __restrict__ counters,
-    int max_units, int slots) {
+    int B, float scale_log2, float* __restrict__ partial, int32_t* __restrict__ counters, int max_units) {
   using C = ACfg<DH>;
   constexpr int DT = C::DT, KS = C::KS, KCH = C::KCH, STAGES = C::STAGES, LOADS = C::LOADS, QG = C::QG, QB = C::QB;
   __shared__ uint4 ring[STAGES][C::STAGE];
   __shared__ int s_last;
 
-  // query tiles over all requests, then units = heads x tiles x splits
+  // query tiles over all requests
   int tiles = 0;
   for (int b = 0; b < B; ++b) tiles += (cu_q[b + 1] - cu_q[b] + QB - 1) / QB;
   if (tiles == 0) return;
-  const int S = choose_kv_split(H * tiles, (max_req_tokens + KB - 1) / KB, slots, max_units);
-  const int units = H * tiles * S;
-  const int per_xcd = (units + kXcds - 1) / kXcds;
+  // tile-steps of one head (key tiles summed over every query tile) and in total
+  long long work_head = 0;
+  for (int b = 0; b < B; ++b)
+    work_head += static_cast<long long>((cu_q[b + 1] - cu_q[b] + QB - 1) / QB) *
+                 ((req_tok_off[b + 1] - req_tok_off[b] + KB - 1) / KB);
+  const long long work = work_head * H;
+  const int G = gridDim.x;
+  // Shares may cut items (partials combined by the last piece to finish) when the
+  // scratch holds two partials per share and every share gets a tile-step;
+  // otherwise every share is a run of whole items.
+  const bool cut = max_units >= 2 * G && work >= static_cast<long long>(G) && G % kXcds == 0;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l32 = lane & 31, lg = lane >> 5;
@@ -189,24 +178,17 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ACfg<D
     v_off[dt] = static_cast<uint32_t>(tr_key * ACfg<DH>::KCH * 16 + ((d_s >> 3) ^ ACfg<DH>::fv(tr_key)) * 16 + (d_s & 7) * 2);
   }
 
-  for (int u = blockIdx.x; u < per_xcd * kXcds; u += gridDim.x) {
-    const int v = (u % kXcds) * per_xcd + u / kXcds;
-    if (v >= units) continue;
-    const int head = v / (tiles * S);
-    const int item = v / S;                       // (head, tile) pair: the split counter's index
-    const int tau = (v / S) % tiles;
-    const int split = v % S;
-    int b = 0, first = 0;
-    for (;; ++b) {
-      const int nt = (cu_q[b + 1] - cu_q[b] + QB - 1) / QB;
-      if (tau < first + nt) break;
-      first += nt;
-    }
+  // One piece of work: key tiles [kt0, kt1) of query tile tau (of request b, whose
+  // first query tile is number `first`) under head `head`; piece `piece` of the
+  // `npieces` that cover this (head, tile) item in key order, the first of them in
+  // share `share0`, whose arrival counter is that share's.
+  auto run_piece = [&](const int head, const int tau, const int b, const int first, const int kt0, const int kt1,
+                       const int piece, const int npieces, const int share0) {
+    // scratch slot of piece j: 2 share0 + 1 for the first, then 2 x (its share)
+    auto slot_of = [&](int j) { return j == 0 ? 2 * share0 + 1 : 2 * (share0 + j); };
     const int q_lo = cu_q[b] + (tau - first) * QB;
     const int q_hi = cu_q[b + 1];
     const int k_beg = req_tok_off[b], k_end = req_tok_off[b + 1];
-    const int n_kv = (k_end - k_beg + KB - 1) / KB;
-    const int kt0 = (split * n_kv) / S, kt1 = ((split + 1) * n_kv) / S;
     const int nkt = kt1 - kt0;
     const size_t col0 = static_cast<size_t>(head) * DH;
     const uint32_t col2 = static_cast<uint32_t>(col0 * 2);
@@ -528,10 +510,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ACfg<D
 #pragma unroll
     for (int g = 0; g < QG; ++g) l_run[g] = half_sum(l_run[g]);
 
-    if (S > 1) {
-      // store this split's unnormalised O, max and sum (lane-major), count the arrival
+    if (npieces > 1) {
+      // store this piece's unnormalised O, max and sum (lane-major), count the arrival
       constexpr int E = QG * (DT * 16 + 2);
-      float* slot = partial + static_cast<size_t>(v) * (E * kThreads) + tid;
+      float* slot = partial + static_cast<size_t>(slot_of(piece)) * (E * kThreads) + tid;
 #pragma unroll
       for (int g = 0; g < QG; ++g) {
 #pragma unroll
@@ -547,28 +529,27 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ACfg<D
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
       __syncthreads();
       if (tid == 0) {
-        const int prev = __hip_atomic_fetch_add(&counters[item], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        s_last = (prev == S - 1);
-        if (prev == S - 1) __hip_atomic_store(&counters[item], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const int prev = __hip_atomic_fetch_add(&counters[share0], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        s_last = (prev == npieces - 1);
+        if (prev == npieces - 1) __hip_atomic_store(&counters[share0], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
       __syncthreads();
-      if (!s_last) continue;
-      // combine the S splits in split order
-      const float* base = partial + static_cast<size_t>(item) * S * (E * kThreads) + tid;
+      if (!s_last) return;
+      // combine the pieces in key order
+      auto piece_base = [&](int j) { return partial + static_cast<size_t>(slot_of(j)) * (E * kThreads) + tid; };
 #pragma unroll
       for (int g = 0; g < QG; ++g) {
         const int mo = (QG * DT * 16 + 2 * g) * kThreads;
         float m_all = -INFINITY;
-        for (int s2 = 0; s2 < S; ++s2)
-          m_all = fmaxf(m_all, __hip_atomic_load(base + static_cast<size_t>(s2) * E * kThreads + mo, __ATOMIC_RELAXED,
-                                                 __HIP_MEMORY_SCOPE_AGENT));
+        for (int s2 = 0; s2 < npieces; ++s2)
+          m_all = fmaxf(m_all, __hip_atomic_load(piece_base(s2) + mo, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
         float l_all = 0.f;
 #pragma unroll
         for (int d = 0; d < DT; ++d)
 #pragma unroll
           for (int r = 0; r < 16; ++r) oacc[g][d][r] = 0.f;
-        for (int s2 = 0; s2 < S; ++s2) {
-          const float* ps = base + static_cast<size_t>(s2) * E * kThreads;
+        for (int s2 = 0; s2 < npieces; ++s2) {
+          const float* ps = piece_base(s2);
           const float ms = __hip_atomic_load(ps + mo, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
           const float w = (ms == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(ms - m_all);
           l_all += w * __hip_atomic_load(ps + mo + kThreads, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
@@ -601,6 +582,70 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ACfg<D
           *reinterpret_cast<uint2*>(orow + d0) = o;
         }
     }
+  };
+
+  // Schedule: the key tiles of every item, items head-major, form one range of
+  // `work` tile-steps cut into G contiguous shares, one per workgroup, numbered so
+  // that each XCD gets consecutive shares (the query tiles of a head share its K/V
+  // in that XCD's L2).  With cuts the shares are equal: a share covers the end of
+  // one item, whole items and the start of another, and an item covered by
+  // several shares is combined by the last of them to finish.  A share w holds
+  // at most two pieces of cut items: the continuation of an item begun in an
+  // earlier share (scratch slot 2w) and the first piece of an item that goes on
+  // into later shares (slot 2w + 1; when that item starts at the share's start
+  // there is no continuation and slot 2w stays unused).  The arrival counter of a
+  // cut item is its first share's.  Without cuts every share boundary is rounded
+  // up to the next item start.
+  const int w = (G % kXcds == 0) ? (blockIdx.x % kXcds) * (G / kXcds) + blockIdx.x / kXcds : static_cast<int>(blockIdx.x);
+  // tile-step q < work: its item's first tile-step and key tiles, head, request,
+  // the request's first query tile and the query tile
+  auto locate = [&](long long q, long long& i_start, int& nkv, int& head, int& b, int& first, int& tau) {
+    head = static_cast<int>(q / work_head);
+    long long r = q - static_cast<long long>(head) * work_head;
+    b = 0;
+    first = 0;
+    nkv = 1;
+    for (; b < B; ++b) {
+      const int nt = (cu_q[b + 1] - cu_q[b] + QB - 1) / QB;
+      nkv = (req_tok_off[b + 1] - req_tok_off[b] + KB - 1) / KB;
+      const long long span = static_cast<long long>(nt) * nkv;
+      if (r < span) break;
+      r -= span;
+      first += nt;
+    }
+    tau = first + static_cast<int>(r / nkv);
+    i_start = q - r % nkv;
+  };
+  auto bound = [&](long long x) -> long long {   // first tile-step of share x (x <= G)
+    const long long q = x * work / G;
+    if (cut || q >= work) return q;
+    long long i_start;
+    int nkv, head, b, first, tau;
+    locate(q, i_start, nkv, head, b, first, tau);
+    return i_start == q ? q : i_start + nkv;
+  };
+  auto share_of = [&](long long q) {   // the share holding tile-step q
+    int x = static_cast<int>(q * G / work);
+    while (x + 1 < G && bound(x + 1) <= q) ++x;
+    return x;
+  };
+  long long p = bound(w);
+  const long long p_end = bound(w + 1);
+  while (p < p_end) {
+    long long i_start;
+    int nkv, head, b, first, tau;
+    locate(p, i_start, nkv, head, b, first, tau);
+    if (b >= B) break;   // unreachable: p < work
+    const long long i_end = i_start + nkv;
+    const int kt0 = static_cast<int>(p - i_start);
+    const int kt1 = static_cast<int>((p_end < i_end ? p_end : i_end) - i_start);
+    int f = w, l = w;
+    if (cut) {
+      f = share_of(i_start);
+      l = share_of(i_end - 1);
+    }
+    run_piece(head, tau, b, first, kt0, kt1, w - f, l - f + 1, f);
+    p = i_start + kt1;
   }
 }
 
@@ -619,16 +664,19 @@ hipError_t launch_attention(const uint16_t* q, const uint16_t* kc, const uint16_
                             int max_req_tokens, float* partial, int32_t* counters, hipStream_t s) {
   const int slots = 2 * num_cus();
   const int max_units = (partial && counters) ? gemm_max_tiles() : 0;
-  // upper bound on the units: every request adds at most one partial query tile
+  // persistent grid: the resident slots, fewer when even one key tile per share
+  // would leave some idle (upper bound on the items: every request adds at most
+  // one partial query tile)
   const int qb = dh >= 128 ? ACfg<128>::QB : ACfg<64>::QB;
   const long long items = static_cast<long long>((n_max + qb - 1) / qb + B) * H;
-  long long grid = items * kMaxKvSplit;
+  long long grid = items * ((max_req_tokens + KB - 1) / KB);
   if (grid > slots) grid = slots;
+  if (grid < 1) grid = 1;
   grid = ((grid + kXcds - 1) / kXcds) * kXcds;
   const float scale_log2 = 1.4426950408889634f / sqrtf(static_cast<float>(dh));
 #define FD_ATTN_LAUNCH(DHV)                                                                                         \
-  attn_fwd_kernel<DHV><<<grid, kThreads, 0, s>>>(q, kc, vc, o, D, H, cu_q, req_tok_off, B, max_req_tokens, scale_log2, \
-                                                 partial, counters, max_units, slots)
+  attn_fwd_kernel<DHV><<<grid, kThreads, 0, s>>>(q, kc, vc, o, D, H, cu_q, req_tok_off, B, scale_log2, partial, counters, \
+                                                 max_units)
   switch (dh) {
     case 16: FD_ATTN_LAUNCH(16); break;
     case 64: FD_ATTN_LAUNCH(64); break;

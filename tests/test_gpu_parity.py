@@ -211,6 +211,39 @@ def test_gemm_tile_shapes_with_ragged_columns():
     gh.compare_step(case, g, o, inp.x_cur, st)
 
 
+def _attention_cuts_items(cu_q, req_tok_off, H, num_cus):
+    """Host mirror of the attention launch's schedule (query tiles of 128, key tiles
+    of 64, a grid of at most two workgroups per CU, 4 * num_cus partial slots): True
+    when the equal per-workgroup shares of the key-tile range may cut (head, query
+    tile) items, whose pieces are then combined by the last one to finish."""
+    QB, KB, slots, max_units = 128, 64, 2 * num_cus, 4 * num_cus
+    act = np.diff(cu_q)
+    tok = np.diff(req_tok_off)
+    nts = [-(-int(a) // QB) for a in act]
+    nkvs = [-(-int(t) // KB) for t in tok]
+    grid = min(((int(tok.sum()) + QB - 1) // QB + len(act)) * H * (-(-int(tok.max()) // KB)), slots)
+    grid = -(-max(grid, 1) // 8) * 8
+    work = H * sum(nt * nk for nt, nk in zip(nts, nkvs))
+    return max_units >= 2 * grid and work >= grid
+
+
+def test_attention_shares_cut_items_varlen():
+    """Three requests of 1024, 2048 and 512 tokens with 384 active rows each (144
+    (head, query tile) items over 8 to 32 key tiles): the attention's equal shares
+    cut items and cross request boundaries, so pieces of one item combine."""
+    reqs = tuple(wl.RequestShape("seq", (n,), (32,)) for n in (1024, 2048, 512))
+    w = small_workload("audio", requests=reqs, activity="count", activity_args=(12,), L=1)
+    case = gh.make_case("audio", workload=w)
+    inp = case.inp
+    g, st = gh.run_gpu(case, inp.eps, inp.x_cur, inp.x_prev)
+    assert g["M"] == 3 * 384
+    ncu = torch.cuda.get_device_properties(0).multi_processor_count
+    assert _attention_cuts_items(g["cu_q"], case.rmap.req_tok_off, w.H, ncu)
+    gh.say(f"attention shares cut items: M={g['M']} cu_q={list(g['cu_q'])} CUs={ncu}")
+    o = gh.run_oracle(case, inp.eps, inp.x_cur, inp.x_prev)
+    gh.compare_step(case, g, o, inp.x_cur, st)
+
+
 def test_single_region_and_single_token_regions():
     reqs = (wl.RequestShape("grid2d", (8, 8), (8, 8)), wl.RequestShape("grid2d", (4, 12), (1, 1)))
     w = small_workload("tiny", requests=reqs, activity="frac", activity_args=(0.3, 0.6), L=1)
