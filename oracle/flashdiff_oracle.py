@@ -29,6 +29,17 @@ What each function follows:
                     come from the cache (Sec. 4 Backend; Prop. "Stale-KV
                     Perturbation").
   latent_update     eq. sf-update with the Euler step of eq. euler.
+  region_importance, importance_update
+                    Sec. 3.2 (Patch Gate, "Adaptive Skipping"): the refinement
+                    importance R_i = |A_i|^-2 sum_{u,v in A_i} SA_uv of a patch,
+                    its change Delta_i = |R_i - Rbar_i| and the last executed
+                    importance Rbar_i, both kept while the patch is skipped.
+                    Readings: SA is the attention of one designated block
+                    averaged over its heads (the paper names one matrix);
+                    Rbar starts at 0, so the first executed step gives
+                    Delta = R; the Delta computed during step t is the gate's
+                    signal at step t + 1 (a patch's queries exist only when it
+                    runs).
 
 Parity pins live in tests/test_oracle_pins.py; no function here is unpinned.
 """
@@ -189,6 +200,48 @@ def attention(q: np.ndarray, k: np.ndarray, v: np.ndarray) -> np.ndarray:
     return p @ v
 
 
+def region_importance(layout: Layout, q: np.ndarray, k_cache: np.ndarray, idx: np.ndarray,
+                      active: np.ndarray, n_heads: int) -> np.ndarray:
+    """Refinement importance of every active region (Sec. 3.2, R_i).
+
+    SA is the self-attention matrix of the block whose queries q [M, D] (rows of
+    the active tokens idx) and key cache k_cache [N, D] are given, averaged over
+    its heads: SA_uv = mean_h softmax_v(q_u,h k_v,h / sqrt(dh)) over the tokens v
+    of u's request.  R_i = |A_i|^-2 sum_{u in A_i} sum_{v in A_i} SA_uv.  Every
+    token of an active region is an active query.  Inactive regions get NaN.
+    """
+    D = q.shape[1]
+    dh = D // n_heads
+    treq = layout.token_request()
+    row_of = {int(u): m for m, u in enumerate(idx)}
+    R = np.full(layout.n_regions, np.nan)
+    for r in range(layout.n_regions):
+        if not active[r]:
+            continue
+        toks = layout.region_tokens(r)
+        b = treq[toks[0]]
+        lo, hi = layout.req_tok_off[b], layout.req_tok_off[b + 1]
+        total = 0.0
+        for hd in range(n_heads):
+            c = slice(hd * dh, (hd + 1) * dh)
+            qr = q[[row_of[int(u)] for u in toks], c]
+            s = qr @ k_cache[lo:hi, c].T / np.sqrt(dh)
+            p = np.exp(s - s.max(axis=1, keepdims=True))
+            p = p / p.sum(axis=1, keepdims=True)
+            total += p[:, toks - lo].sum()
+        R[r] = total / n_heads / len(toks) ** 2
+    return R
+
+
+def importance_update(R: np.ndarray, active: np.ndarray, r_bar: np.ndarray, delta: np.ndarray):
+    """Delta_i = |R_i - Rbar_i| and Rbar_i = R_i for the executed (active) regions;
+    a skipped region keeps both (Sec. 3.2).  Returns (Rbar', Delta')."""
+    act = active.astype(bool)
+    r_new = np.where(act, R, r_bar)
+    d_new = np.where(act, np.abs(np.where(act, R, 0.0) - r_bar), delta)
+    return r_new.astype(np.float64), d_new.astype(np.float64)
+
+
 def embed(xa: np.ndarray, idx: np.ndarray, w_e: np.ndarray, b_e: np.ndarray, pos: np.ndarray) -> np.ndarray:
     """Token embedding of the gathered latent rows: xa W_e^T + b_e + pos[token]."""
     return xa @ w_e.T + b_e + pos[idx]
@@ -196,7 +249,8 @@ def embed(xa: np.ndarray, idx: np.ndarray, w_e: np.ndarray, b_e: np.ndarray, pos
 
 def block_forward(h: np.ndarray, idx: np.ndarray, row_req: np.ndarray, layout: Layout,
                   blk: Dict[str, np.ndarray], cond: np.ndarray, k_cache: np.ndarray,
-                  v_cache: np.ndarray, n_heads: int, out_rows: Optional[np.ndarray] = None) -> np.ndarray:
+                  v_cache: np.ndarray, n_heads: int, out_rows: Optional[np.ndarray] = None,
+                  importance: Optional[dict] = None) -> np.ndarray:
     """One adaLN DiT block on the active rows h [M, D] (token ids idx, requests row_req).
 
     k_cache / v_cache [N, D] are updated in place: the rows of the active tokens
@@ -205,6 +259,9 @@ def block_forward(h: np.ndarray, idx: np.ndarray, row_req: np.ndarray, layout: L
     query attends to every token of its own request.  Once the caches are
     written the rows are independent, so `out_rows` (indices into the M rows)
     restricts the rest of the block to those rows and returns only them.
+    `importance`, when given, is a dict with the region map's `layout`-level
+    inputs 'active' (bool [R]); it receives 'R', the region importance of this
+    block's self-attention (region_importance).
     """
     M, D = h.shape
     dh = D // n_heads
@@ -214,6 +271,8 @@ def block_forward(h: np.ndarray, idx: np.ndarray, row_req: np.ndarray, layout: L
     q, k, v = qkv[:, :D], qkv[:, D:2 * D], qkv[:, 2 * D:]
     k_cache[idx] = k
     v_cache[idx] = v
+    if importance is not None:
+        importance["R"] = region_importance(layout, q, k_cache, idx, importance["active"], n_heads)
     if out_rows is not None:
         h, q, row_req = h[out_rows], q[out_rows], row_req[out_rows]
         M = len(out_rows)
@@ -273,10 +332,12 @@ class GateState:
     s_tilde: np.ndarray      # fp64 [R] frozen change
     skip_run: np.ndarray     # int32 [R] consecutive skips
     active: np.ndarray       # bool [R] previous decision
+    r_bar: Optional[np.ndarray] = None   # fp64 [R] importance when last executed
+    delta: Optional[np.ndarray] = None   # fp64 [R] importance change (the next step's signal)
 
     @staticmethod
     def fresh(R: int) -> "GateState":
-        return GateState(np.zeros(R), np.zeros(R, np.int32), np.ones(R, bool))
+        return GateState(np.zeros(R), np.zeros(R, np.int32), np.ones(R, bool), np.zeros(R), np.zeros(R))
 
 
 def params_block(params: Dict[str, np.ndarray], l: int) -> Dict[str, np.ndarray]:
@@ -288,7 +349,8 @@ def sparse_step(layout: Layout, params: Dict[str, np.ndarray], n_heads: int, con
                 x_cur: np.ndarray, x_prev: np.ndarray, gate: GateState, eps: np.ndarray,
                 eta: float, max_skip: int, k_cache: List[np.ndarray], v_cache: List[np.ndarray],
                 vcache: np.ndarray, dt: np.ndarray, skip_mode: int = FREEZE, n_layers: Optional[int] = None,
-                sample_rows: Optional[np.ndarray] = None):
+                sample_rows: Optional[np.ndarray] = None, signal: str = "delta",
+                importance_block: Optional[int] = None):
     """One region-sparse denoising step (score, gate, gather, blocks, update).
 
     params holds float64 arrays: per-block w_*/b_* stacked on axis 0, plus
@@ -299,8 +361,16 @@ def sparse_step(layout: Layout, params: Dict[str, np.ndarray], n_heads: int, con
     sample_rows (indices into the M active rows) restricts the last block, the
     final layer and the active-row update to those rows: h and v then hold only
     them, and x is updated only on their tokens (and on skipped tokens).
+
+    signal selects the gate's per-region signal: "delta" (the latent activity of
+    region_score) or "importance" (the importance change Delta carried in the
+    gate state from the previous step).  importance_block (a block index) makes
+    that block's self-attention update Rbar and Delta for the next step.
     """
-    score = region_score(layout, x_cur, x_prev)
+    if signal == "importance":
+        score = np.array(gate.delta, dtype=np.float64, copy=True)
+    else:
+        score = region_score(layout, x_cur, x_prev)
     s_t, run, active = gate_select(layout, score, gate.s_tilde, gate.skip_run, gate.active,
                                    eps, eta, max_skip)
     idx, cu = active_rows(layout, active)
@@ -309,14 +379,22 @@ def sparse_step(layout: Layout, params: Dict[str, np.ndarray], n_heads: int, con
     h = embed(xa, idx, params["w_e"], params["b_e"], params["pos"])
     L = params["w_qkv"].shape[0] if n_layers is None else n_layers
     rows = np.arange(len(idx)) if sample_rows is None else np.asarray(sample_rows)
+    imp = None
     for l in range(L):
         last = sample_rows is not None and l == L - 1
+        hook = dict(active=active) if importance_block == l else None
         h = block_forward(h, idx, row_req, layout, params_block(params, l), cond,
-                          k_cache[l], v_cache[l], n_heads, out_rows=rows if last else None)
+                          k_cache[l], v_cache[l], n_heads, out_rows=rows if last else None,
+                          importance=hook)
+        if hook is not None:
+            imp = hook["R"]
+    r_bar, delta = gate.r_bar, gate.delta
+    if imp is not None:
+        r_bar, delta = importance_update(imp, active, gate.r_bar, gate.delta)
     if sample_rows is not None and L == 0:
         h = h[rows]
     v = final_layer(h, row_req[rows], params["w_adaf"], params["b_adaf"], params["w_out"],
                     params["b_out"], cond)
     x_new, vc_new = latent_update(x_cur, v, idx[rows], layout, dt, vcache, active, skip_mode)
     return dict(score=score, active=active, idx=idx, cu_q=cu, h=h, v=v, x=x_new, vcache=vc_new,
-                gate=GateState(s_t, run, active), rows=rows)
+                gate=GateState(s_t, run, active, r_bar, delta), rows=rows, importance=imp)

@@ -393,3 +393,116 @@ def test_designed_workloads_realise_their_active_sets():
             rr = lay.region_request()
             margin = np.abs(wts - inp.eps[rr]) / np.maximum(inp.eps[rr], 1e-300)
             assert margin[inp.eps[rr] > 0].min() > 0.05
+
+
+# ------------------------------------------------------------------ refinement importance (Sec. 3.2)
+
+def _importance_setup(seed, B=3, H=2, dh=4, max_regions=4, max_tokens=4):
+    rng = np.random.default_rng(seed)
+    lay = random_gate_layout(rng, B=B, max_regions=max_regions, max_tokens=max_tokens)
+    N = int(lay.req_tok_off[-1])
+    active = rng.random(lay.n_regions) < 0.6
+    active[0] = True
+    idx, _ = orc.active_rows(lay, active)
+    q = rng.standard_normal((len(idx), H * dh))
+    k = rng.standard_normal((N, H * dh))
+    return rng, lay, active, idx, q, k
+
+
+def test_importance_bruteforce_loops():
+    """R_i from the self-attention matrix written out element by element."""
+    rng, lay, active, idx, q, k = _importance_setup(11)
+    H, dh = 2, 4
+    R = orc.region_importance(lay, q, k, idx, active, H)
+    treq = lay.token_request()
+    row_of = {int(u): m for m, u in enumerate(idx)}
+    for r in range(lay.n_regions):
+        if not active[r]:
+            assert math.isnan(R[r])
+            continue
+        toks = [u for u in range(len(lay.token_region)) if lay.token_region[u] == r]
+        b = treq[toks[0]]
+        keys = list(range(lay.req_tok_off[b], lay.req_tok_off[b + 1]))
+        acc = 0.0
+        for u in toks:
+            for hd in range(H):
+                sc = [sum(q[row_of[u], hd * dh + d] * k[v, hd * dh + d] for d in range(dh)) / math.sqrt(dh) for v in keys]
+                mx = max(sc)
+                ex = [math.exp(x - mx) for x in sc]
+                z = sum(ex)
+                for j, v in enumerate(keys):
+                    if lay.token_region[v] == r:
+                        acc += ex[j] / z / H
+        assert abs(R[r] - acc / len(toks) ** 2) <= 1e-12 * max(1.0, abs(acc))
+
+
+def test_importance_uniform_attention_closed_form():
+    """All scores equal (q = 0): SA_uv = 1/N_b, so R_i = 1/N_b for every active region."""
+    rng, lay, active, idx, q, k = _importance_setup(12, B=4)
+    R = orc.region_importance(lay, np.zeros_like(q), k, idx, active, 2)
+    treq = lay.token_request()
+    for r in range(lay.n_regions):
+        if active[r]:
+            b = treq[lay.region_tokens(r)[0]]
+            nb = lay.req_tok_off[b + 1] - lay.req_tok_off[b]
+            assert R[r] == pytest.approx(1.0 / nb, rel=1e-12)
+
+
+def test_importance_one_region_request_and_block_diagonal_limit():
+    """A region that is its whole request: each attention row sums to one over it,
+    so R = 1/|A|.  Queries and keys that score 30 inside a region and 0 across
+    regions: SA is block diagonal up to e^-30, so R_i -> 1/|A_i|."""
+    lay = orc.Layout(np.array([0, 0, 0, 0, 0, 1, 1, 2, 2, 2], np.int64), np.array([0, 5, 10], np.int64), 3)
+    active = np.ones(3, bool)
+    idx, _ = orc.active_rows(lay, active)
+    rng = np.random.default_rng(13)
+    H, dh = 2, 3
+    q = rng.standard_normal((10, H * dh))
+    k = rng.standard_normal((10, H * dh))
+    R = orc.region_importance(lay, q, k, idx, active, H)
+    assert R[0] == pytest.approx(1.0 / 5, rel=1e-12)
+    onehot = np.zeros((10, H * dh))
+    for u, r in enumerate(lay.token_region):
+        for hd in range(H):
+            onehot[u, hd * dh + r] = math.sqrt(30.0 * math.sqrt(dh))
+    R = orc.region_importance(lay, onehot, onehot, idx, active, H)
+    for r, n in ((0, 5), (1, 2), (2, 3)):
+        assert R[r] == pytest.approx(1.0 / n, rel=1e-9)
+
+
+def test_importance_update_rule():
+    """Executed regions: Delta = |R - Rbar| and Rbar = R; skipped ones keep both."""
+    R = np.array([0.5, np.nan, 0.1, 0.3])
+    active = np.array([True, False, True, True])
+    r_bar = np.array([0.2, 0.7, 0.4, 0.3])
+    delta = np.array([9.0, 0.25, 9.0, 9.0])
+    rb, d = orc.importance_update(R, active, r_bar, delta)
+    np.testing.assert_array_equal(rb, [0.5, 0.7, 0.1, 0.3])
+    np.testing.assert_array_equal(d, [0.5 - 0.2, 0.25, abs(0.1 - 0.4), 0.0])
+
+
+def test_importance_signal_drives_the_next_gate():
+    """In importance mode the gate thresholds the Delta carried in from the previous
+    step (not the latent activity), and the designated block's importance updates
+    Rbar/Delta of the executed regions only."""
+    w = wl.WORKLOADS["tiny"]
+    lay = oracle_layout(w)
+    params = params_f64(wl.make_params(w))
+    cond = wl.make_cond(w).double().numpy()
+    inp = wl.step_inputs(w, 0)
+    kc, vc = wl.make_kv_cache(w)
+    kc = [c.double().numpy() for c in kc]
+    vc = [c.double().numpy() for c in vc]
+    gate = orc.GateState.fresh(w.R)
+    gate.delta = np.arange(1.0, w.R + 1.0)            # region r carries Delta = r + 1
+    gate.r_bar = np.full(w.R, 0.01)
+    eps = np.array([(w.R / 2 + 0.5) / gate.delta.sum()])   # active iff r + 1 > R/2 + 0.5
+    o = orc.sparse_step(lay, params, w.H, cond, inp.x_cur, inp.x_prev, gate, eps, 0.0, 0, kc, vc,
+                        np.zeros_like(inp.x_cur), wl.dt_per_request(w), signal="importance",
+                        importance_block=0)
+    np.testing.assert_array_equal(o["active"], np.arange(w.R) + 1 > w.R / 2 + 0.5)
+    act = o["active"]
+    np.testing.assert_array_equal(o["gate"].r_bar[~act], 0.01)
+    np.testing.assert_array_equal(o["gate"].delta[~act], gate.delta[~act])
+    np.testing.assert_allclose(o["gate"].r_bar[act], o["importance"][act], rtol=0)
+    np.testing.assert_allclose(o["gate"].delta[act], np.abs(o["importance"][act] - 0.01), rtol=0)
