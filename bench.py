@@ -54,6 +54,33 @@ def kernel_flops(name: str, w, M: int) -> float:
             "final": 2.0 * M * D * C}.get(name, 0.0)
 
 
+def importance_cost(fdl, stp, run, w, M: int, i: int) -> dict:
+    """Untimed: one step with the paper's importance signal computed from the last
+    block's self-attention, the importance call bracketed by the library's event
+    timer.  Flops: the |A_r|^2 in-region scores of every active region and head."""
+    torch = sys.modules["torch"]
+    orig = stp.step
+
+    def step_imp(*a, **k):
+        k["importance_block"] = w.L - 1
+        return orig(*a, **k)
+
+    stp.step = step_imp
+    fdl.fd_timer_arm("importance", 8)
+    run(i)
+    torch.cuda.synchronize()
+    ms = fdl.fd_timer_read(8)
+    fdl.fd_timer_disarm()
+    stp.step = orig
+    n_act = int(stp.active.sum().item())
+    region_tokens = M / max(n_act, 1)
+    flops = n_act * region_tokens * region_tokens * w.H * 2.0 * w.dh
+    us = float(ms.sum()) * 1e3
+    return {"when": "once per step with the importance gate signal (not in the timed step)",
+            "block": w.L - 1, "active_regions": n_act, "us": us, "flops": flops,
+            "achieved_tflops": flops / (us * 1e-6) / 1e12 if us > 0 else None}
+
+
 def kernel_bytes(name: str, w, M: int) -> float:
     """Algorithmic HBM bytes of one launch of a streaming kernel."""
     C, N = w.C, w.N
@@ -264,7 +291,7 @@ def main():
 
     # per-kernel time per step (untimed calibration pass, one kernel type at a time)
     per_kernel = {}
-    for name in fdl.KERNELS:
+    for name in (k for k in fdl.KERNELS if k != "importance"):
         fdl.fd_timer_arm(name, 4 * w.L + 8)
         run(0)
         torch.cuda.synchronize()
@@ -313,6 +340,7 @@ def main():
                      "launches": len(dom_ms), "avg_ms": dom_avg_ms},
         "kernels_ms_per_step": {k: round(v[0], 4) for k, v in per_kernel.items()},
     }
+    out["importance"] = importance_cost(fdl, stp, run, w, M, args.warmup + args.steps)
     if not args.no_hbm:
         print("[bench] streaming-kernel bandwidth (score, gather, scatter)", file=sys.stderr, flush=True)
         out["hbm"] = hbm_streams(torch, fdl, wl)

@@ -16,6 +16,10 @@
  *   fd_final          -> velocity rows
  *   fd_scatter_update -> Euler update of the latent          (eq. sf-update)
  *
+ * With the paper's own gate signal, fd_region_importance runs after the block
+ * chosen to supply the self-attention, and its Delta replaces the region score
+ * at the next step's fd_select (Sec. 3.2, refinement importance).
+ *
  * Conventions for every entry point:
  *  - Pointers named in "device" are HIP device pointers; all other pointers are
  *    host pointers.  All device buffers are owned by the caller; the library
@@ -220,13 +224,41 @@ fd_status fd_adaln(const fd_dims* dims, int32_t n_blocks, int32_t n_out, int32_t
  *   h        device fp32 [N][D], rows < *m updated in place
  *   idx, cu_q, m  from fd_select
  *   k_cache, v_cache  device bf16 [N][D] of this block (head h at columns h*dh..)
- *   ws       device scratch of fd_block_ws_size bytes, 256-byte aligned
+ *   ws       device scratch of fd_block_ws_size bytes, 256-byte aligned; after
+ *            the call it holds this block's queries and per-query softmax
+ *            normalisers, which fd_region_importance reads
  */
 size_t fd_block_ws_size(const fd_plan* plan, const fd_dims* dims);
 fd_status fd_block_forward(const fd_plan* plan, const fd_dims* dims, const fd_block_weights* w,
                            const float* cond, float* h, const int32_t* idx, const int32_t* cu_q,
                            const int32_t* m, uint16_t* k_cache, uint16_t* v_cache, void* ws,
                            size_t ws_bytes, fd_stream_t stream);
+
+/* ---------------------------------------------------------------- importance
+ * The Patch Gate's own signal (Sec. 3.2, refinement importance, Alg. 1
+ * PatchGate): for every active region i,
+ *   R_i = |A_i|^-2 sum_{u,v in A_i} SA_uv,
+ * SA the self-attention matrix of one block averaged over its H heads (SA_uv =
+ * mean_h softmax over the tokens of u's request); then Delta_i = |R_i - Rbar_i|
+ * and Rbar_i = R_i.  Skipped regions keep Rbar and Delta (their queries do not
+ * run).  Passing Delta as `score` to the next step's fd_select gates on it.
+ * Call right after fd_block_forward of the chosen block, with the workspace
+ * that call used: it reads that call's queries and per-query softmax
+ * normalisers from it, and the block's key cache as that call left it.
+ *   block_ws, block_ws_bytes  device, the fd_block_forward workspace (not reused since)
+ *   k_cache      device bf16 [N][D], the block's key cache
+ *   idx, m       device, the active rows of fd_select
+ *   active       device uint8 [R], this step's mask
+ *   r_bar, delta device fp64 [R], updated in place (both 0 before the first step)
+ *   importance   optional device fp64 [R]: R_i of active regions, NaN for skipped ones
+ *   ws           device scratch of fd_importance_ws_size bytes, 256-byte aligned
+ * FD_E_UNSUPPORTED when a region's key rows of one head exceed 156 KB of LDS.
+ */
+size_t fd_importance_ws_size(const fd_plan* plan, const fd_dims* dims);
+fd_status fd_region_importance(const fd_plan* plan, const fd_dims* dims, const void* block_ws,
+                               size_t block_ws_bytes, const uint16_t* k_cache, const int32_t* idx,
+                               const int32_t* m, const uint8_t* active, double* r_bar, double* delta,
+                               double* importance, void* ws, size_t ws_bytes, fd_stream_t stream);
 
 /* ---------------------------------------------------------------- final
  * v[i] = (LN(h_i) * (1 + scale) + shift) W_out^T + b_out, (shift, scale) =
@@ -261,7 +293,7 @@ fd_status fd_scatter_update(const fd_plan* plan, int32_t C, float* x, const floa
 enum {
   FD_K_SCORE = 1, FD_K_SELECT, FD_K_GATHER, FD_K_EMBED, FD_K_ADALN, FD_K_LN,
   FD_K_GEMM_QKV, FD_K_ATTN, FD_K_GEMM_O, FD_K_GEMM_MLP1, FD_K_GEMM_MLP2,
-  FD_K_FINAL, FD_K_SCATTER
+  FD_K_FINAL, FD_K_SCATTER, FD_K_IMPORTANCE
 };
 fd_status fd_timer_arm(int32_t kernel, int32_t capacity);
 int32_t fd_timer_read(float* ms, int32_t capacity);

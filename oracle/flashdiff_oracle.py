@@ -201,21 +201,22 @@ def attention(q: np.ndarray, k: np.ndarray, v: np.ndarray) -> np.ndarray:
 
 
 def region_importance(layout: Layout, q: np.ndarray, k_cache: np.ndarray, idx: np.ndarray,
-                      active: np.ndarray, n_heads: int) -> np.ndarray:
+                      active: np.ndarray, n_heads: int, regions: Optional[np.ndarray] = None) -> np.ndarray:
     """Refinement importance of every active region (Sec. 3.2, R_i).
 
     SA is the self-attention matrix of the block whose queries q [M, D] (rows of
     the active tokens idx) and key cache k_cache [N, D] are given, averaged over
     its heads: SA_uv = mean_h softmax_v(q_u,h k_v,h / sqrt(dh)) over the tokens v
     of u's request.  R_i = |A_i|^-2 sum_{u in A_i} sum_{v in A_i} SA_uv.  Every
-    token of an active region is an active query.  Inactive regions get NaN.
+    token of an active region is an active query.  Inactive regions get NaN, and
+    so do active ones outside `regions` when that subset is given.
     """
     D = q.shape[1]
     dh = D // n_heads
     treq = layout.token_request()
     row_of = {int(u): m for m, u in enumerate(idx)}
     R = np.full(layout.n_regions, np.nan)
-    for r in range(layout.n_regions):
+    for r in (range(layout.n_regions) if regions is None else regions):
         if not active[r]:
             continue
         toks = layout.region_tokens(r)
@@ -272,7 +273,8 @@ def block_forward(h: np.ndarray, idx: np.ndarray, row_req: np.ndarray, layout: L
     k_cache[idx] = k
     v_cache[idx] = v
     if importance is not None:
-        importance["R"] = region_importance(layout, q, k_cache, idx, importance["active"], n_heads)
+        importance["R"] = region_importance(layout, q, k_cache, idx, importance["active"], n_heads,
+                                            importance.get("regions"))
     if out_rows is not None:
         h, q, row_req = h[out_rows], q[out_rows], row_req[out_rows]
         M = len(out_rows)
@@ -350,7 +352,7 @@ def sparse_step(layout: Layout, params: Dict[str, np.ndarray], n_heads: int, con
                 eta: float, max_skip: int, k_cache: List[np.ndarray], v_cache: List[np.ndarray],
                 vcache: np.ndarray, dt: np.ndarray, skip_mode: int = FREEZE, n_layers: Optional[int] = None,
                 sample_rows: Optional[np.ndarray] = None, signal: str = "delta",
-                importance_block: Optional[int] = None):
+                importance_block: Optional[int] = None, importance_regions: Optional[np.ndarray] = None):
     """One region-sparse denoising step (score, gate, gather, blocks, update).
 
     params holds float64 arrays: per-block w_*/b_* stacked on axis 0, plus
@@ -365,7 +367,9 @@ def sparse_step(layout: Layout, params: Dict[str, np.ndarray], n_heads: int, con
     signal selects the gate's per-region signal: "delta" (the latent activity of
     region_score) or "importance" (the importance change Delta carried in the
     gate state from the previous step).  importance_block (a block index) makes
-    that block's self-attention update Rbar and Delta for the next step.
+    that block's self-attention update Rbar and Delta for the next step
+    (importance_regions restricts the importance to a subset of the regions;
+    the others then read NaN and the state update is left to the caller).
     """
     if signal == "importance":
         score = np.array(gate.delta, dtype=np.float64, copy=True)
@@ -382,14 +386,14 @@ def sparse_step(layout: Layout, params: Dict[str, np.ndarray], n_heads: int, con
     imp = None
     for l in range(L):
         last = sample_rows is not None and l == L - 1
-        hook = dict(active=active) if importance_block == l else None
+        hook = dict(active=active, regions=importance_regions) if importance_block == l else None
         h = block_forward(h, idx, row_req, layout, params_block(params, l), cond,
                           k_cache[l], v_cache[l], n_heads, out_rows=rows if last else None,
                           importance=hook)
         if hook is not None:
             imp = hook["R"]
     r_bar, delta = gate.r_bar, gate.delta
-    if imp is not None:
+    if imp is not None and importance_regions is None:
         r_bar, delta = importance_update(imp, active, gate.r_bar, gate.delta)
     if sample_rows is not None and L == 0:
         h = h[rows]

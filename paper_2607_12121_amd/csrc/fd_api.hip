@@ -29,6 +29,7 @@ struct BlockWs {
   uint16_t* g;
   float* partial;      // split-K partial tiles
   int32_t* counters;   // split-K arrival counters (zeroed at the start of every block)
+  float* lse;          // [N][H] base-2 log-sum-exp of each active query's scaled scores
   size_t bytes;
 };
 
@@ -52,6 +53,7 @@ BlockWs carve_block_ws(const fd_plan* p, const fd_dims* d, void* base) {
   const size_t attn_part = fdh::attn_scratch_bytes(d->dh);
   w.partial = static_cast<float*>(take(gemm_part > attn_part ? gemm_part : attn_part));
   w.counters = static_cast<int32_t*>(take(tiles * sizeof(int32_t)));
+  w.lse = static_cast<float*>(take(n * d->H * sizeof(float)));
   w.bytes = off;
   return w;
 }
@@ -334,7 +336,7 @@ fd_status fd_block_forward(const fd_plan* plan, const fd_dims* dims, const fd_bl
   FD_LAUNCH(FD_K_GEMM_QKV, s, fdh::launch_gemm(fdh::GEMM_QKV, g, s));
   FD_LAUNCH(FD_K_ATTN, s,
             fdh::launch_attention(bw.q, k_cache, v_cache, bw.o, D, dims->H, dims->dh, cu_q, plan->req_tok_off, B, N,
-                                  plan->max_request_tokens, bw.partial, bw.counters, s));
+                                  plan->max_request_tokens, bw.partial, bw.counters, bw.lse, s));
   g = fdh::GemmArgs{};
   g.n_max = N; g.m = m; g.idx = idx; g.cu_q = cu_q; g.n_req = B; g.D = D;
   g.partial = bw.partial; g.counters = bw.counters; g.max_units = fdh::gemm_max_tiles();
@@ -353,6 +355,38 @@ fd_status fd_block_forward(const fd_plan* plan, const fd_dims* dims, const fd_bl
   g.act = bw.g; g.wt = w->w_2; g.bias = w->b_2; g.N = D; g.K = F;
   g.out_f32 = h; g.gate = mod + 5 * D; g.gate_stride = 6 * D;
   FD_LAUNCH(FD_K_GEMM_MLP2, s, fdh::launch_gemm(fdh::GEMM_RESID, g, s));
+  return FD_OK;
+}
+
+size_t fd_importance_ws_size(const fd_plan* plan, const fd_dims* dims) {
+  if (!plan || !dims) return 0;
+  return align_up(static_cast<size_t>(plan->n_tokens) * sizeof(int32_t)) +
+         align_up(static_cast<size_t>(plan->n_regions) * dims->H * sizeof(float));
+}
+
+fd_status fd_region_importance(const fd_plan* plan, const fd_dims* dims, const void* block_ws, size_t block_ws_bytes,
+                               const uint16_t* k_cache, const int32_t* idx, const int32_t* m, const uint8_t* active,
+                               double* r_bar, double* delta, double* importance, void* ws, size_t ws_bytes,
+                               fd_stream_t stream) {
+  FD_TRY(check_plan(plan));
+  FD_TRY(check_dims(dims));
+  FD_REQUIRE(block_ws && k_cache && idx && m && active && r_bar && delta && ws, "null pointer");
+  FD_REQUIRE(aligned(block_ws, kAlign) && aligned(ws, kAlign) && aligned(k_cache, 16), "misaligned buffer");
+  const BlockWs bw = carve_block_ws(plan, dims, const_cast<void*>(block_ws));
+  if (block_ws_bytes < bw.bytes)
+    return fdh::set_error("block workspace too small (%zu < %zu)", block_ws_bytes, bw.bytes), FD_E_SHAPE;
+  const size_t need = fd_importance_ws_size(plan, dims);
+  if (ws_bytes < need) return fdh::set_error("importance workspace too small (%zu < %zu)", ws_bytes, need), FD_E_SHAPE;
+  if (fdh::importance_lds_bytes(dims->dh, plan->max_region_tokens) > 156 * 1024)
+    return fdh::set_error("regions of %d tokens exceed the importance kernel's LDS staging", plan->max_region_tokens),
+           FD_E_UNSUPPORTED;
+  const uintptr_t b0 = reinterpret_cast<uintptr_t>(ws);
+  int32_t* pos = reinterpret_cast<int32_t*>(b0);
+  float* part = reinterpret_cast<float*>(b0 + align_up(static_cast<size_t>(plan->n_tokens) * sizeof(int32_t)));
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  FD_LAUNCH(FD_K_IMPORTANCE, s,
+            fdh::launch_importance(plan, dims->D, dims->H, dims->dh, idx, m, active, bw.q, k_cache, bw.lse, pos, part,
+                                   r_bar, delta, importance, s));
   return FD_OK;
 }
 
@@ -393,7 +427,7 @@ fd_status fd_scatter_update(const fd_plan* plan, int32_t C, float* x, const floa
 }
 
 fd_status fd_timer_arm(int32_t kernel, int32_t capacity) {
-  FD_REQUIRE(kernel >= FD_K_SCORE && kernel <= FD_K_SCATTER && capacity >= 1 && capacity <= (1 << 20),
+  FD_REQUIRE(kernel >= FD_K_SCORE && kernel <= FD_K_IMPORTANCE && capacity >= 1 && capacity <= (1 << 20),
              "bad timer arguments");
   std::lock_guard<std::mutex> lk(g_timer.mu);
   for (hipEvent_t e : g_timer.ev) (void)hipEventDestroy(e);

@@ -126,7 +126,14 @@ hipError_t launch_gemm(GemmKind kind, const GemmArgs& a, hipStream_t s);
 
 hipError_t launch_attention(const uint16_t* q, const uint16_t* kc, const uint16_t* vc, uint16_t* o, int D, int H,
                             int dh, const int32_t* cu_q, const int32_t* req_tok_off, int B, int n_max,
-                            int max_req_tokens, float* partial, int32_t* counters, hipStream_t s);
+                            int max_req_tokens, float* partial, int32_t* counters, float* lse, hipStream_t s);
+// Region importance (pos: active row of every token, part: [R][H] partial sums).
+size_t importance_lds_bytes(int dh, int max_region_tokens);
+hipError_t launch_importance(const fd_plan* p, int D, int H, int dh, const int32_t* idx, const int32_t* m,
+                             const uint8_t* active, const uint16_t* q, const uint16_t* kc, const float* lse,
+                             int32_t* pos, float* part, double* r_bar, double* delta, double* importance,
+                             hipStream_t s);
+
 // Bytes of KV-split scratch the attention kernel needs for head dim dh.
 size_t attn_scratch_bytes(int dh);
 

@@ -131,7 +131,8 @@ template <int DH>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ACfg<DH>::OCC, ACfg<DH>::OCC))) void attn_fwd_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ Kc, const uint16_t* __restrict__ Vc,
     uint16_t* __restrict__ O, int D, int H, const int32_t* __restrict__ cu_q, const int32_t* __restrict__ req_tok_off,
-    int B, float scale_log2, float* __restrict__ partial, int32_t* __restrict__ counters, int max_units) {
+    int B, float scale_log2, float* __restrict__ partial, int32_t* __restrict__ counters, int max_units,
+    float* __restrict__ lse) {
   using C = ACfg<DH>;
   constexpr int DT = C::DT, KS = C::KS, KCH = C::KCH, STAGES = C::STAGES, LOADS = C::LOADS, QG = C::QG, QB = C::QB;
   __shared__ uint4 ring[STAGES][C::STAGE];
@@ -550,17 +551,24 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ACfg<D
           for (int r = 0; r < 16; ++r) oacc[g][d][r] = 0.f;
         for (int s2 = 0; s2 < npieces; ++s2) {
           const float* ps = piece_base(s2);
+          // every load of the piece in flight before the first use (the
+          // scheduler would otherwise trade them for registers, one latency each)
+          float pv[DT * 16];
+#pragma unroll
+          for (int e = 0; e < DT * 16; ++e)
+            pv[e] = __hip_atomic_load(ps + (g * DT * 16 + e) * kThreads, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
           const float ms = __hip_atomic_load(ps + mo, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          const float ls = __hip_atomic_load(ps + mo + kThreads, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          __builtin_amdgcn_sched_barrier(0);
           const float w = (ms == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(ms - m_all);
-          l_all += w * __hip_atomic_load(ps + mo + kThreads, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          l_all += w * ls;
 #pragma unroll
           for (int d = 0; d < DT; ++d)
 #pragma unroll
-            for (int r = 0; r < 16; ++r)
-              oacc[g][d][r] += w * __hip_atomic_load(ps + ((g * DT + d) * 16 + r) * kThreads, __ATOMIC_RELAXED,
-                                                     __HIP_MEMORY_SCOPE_AGENT);
+            for (int r = 0; r < 16; ++r) oacc[g][d][r] += w * pv[d * 16 + r];
         }
         l_run[g] = l_all;
+        m_run[g] = m_all;
       }
     }
 
@@ -568,6 +576,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ACfg<D
     for (int g = 0; g < QG; ++g) {
       const int qrow = q_lo + wave * (32 * QG) + g * 32 + l32;
       if (qrow >= q_hi) continue;
+      // base-2 log-sum-exp of the scaled scores: softmax = exp2(s * scale_log2 - lse)
+      if (lse && lg == 0) lse[static_cast<size_t>(qrow) * H + head] = m_run[g] + __log2f(l_run[g]);
       const float inv_l = 1.0f / l_run[g];
       uint16_t* orow = O + static_cast<size_t>(qrow) * D + col0;
 #pragma unroll
@@ -661,7 +671,7 @@ size_t attn_scratch_bytes(int dh) {
 
 hipError_t launch_attention(const uint16_t* q, const uint16_t* kc, const uint16_t* vc, uint16_t* o, int D, int H,
                             int dh, const int32_t* cu_q, const int32_t* req_tok_off, int B, int n_max,
-                            int max_req_tokens, float* partial, int32_t* counters, hipStream_t s) {
+                            int max_req_tokens, float* partial, int32_t* counters, float* lse, hipStream_t s) {
   const int slots = 2 * num_cus();
   const int max_units = (partial && counters) ? gemm_max_tiles() : 0;
   // persistent grid: the resident slots, fewer when even one key tile per share
@@ -676,7 +686,7 @@ hipError_t launch_attention(const uint16_t* q, const uint16_t* kc, const uint16_
   const float scale_log2 = 1.4426950408889634f / sqrtf(static_cast<float>(dh));
 #define FD_ATTN_LAUNCH(DHV)                                                                                         \
   attn_fwd_kernel<DHV><<<grid, kThreads, 0, s>>>(q, kc, vc, o, D, H, cu_q, req_tok_off, B, scale_log2, partial, counters, \
-                                                 max_units)
+                                                 max_units, lse)
   switch (dh) {
     case 16: FD_ATTN_LAUNCH(16); break;
     case 64: FD_ATTN_LAUNCH(64); break;

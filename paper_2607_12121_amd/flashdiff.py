@@ -23,7 +23,8 @@ FD_SKIP_FREEZE = 0
 FD_SKIP_REUSE_DRIFT = 1
 
 KERNELS = {"score": 1, "select": 2, "gather": 3, "embed": 4, "adaln": 5, "ln": 6, "gemm_qkv": 7,
-           "attn": 8, "gemm_o": 9, "gemm_mlp1": 10, "gemm_mlp2": 11, "final": 12, "scatter": 13}
+           "attn": 8, "gemm_o": 9, "gemm_mlp1": 10, "gemm_mlp2": 11, "final": 12, "scatter": 13,
+           "importance": 14}
 
 _p = ctypes.c_void_p
 _i32 = ctypes.c_int32
@@ -85,6 +86,9 @@ def lib() -> ctypes.CDLL:
         "fd_final": ([P(FdPlan), P(FdDims), P(FdFinalWeights), _p, _p, _p, _p, _p, _p, ctypes.c_size_t, _p],
                      _i32),
         "fd_scatter_update": ([P(FdPlan), _i32, _p, _p, _p, _p, _p, _p, _p, _i32, _p], _i32),
+        "fd_importance_ws_size": ([P(FdPlan), P(FdDims)], ctypes.c_size_t),
+        "fd_region_importance": ([P(FdPlan), P(FdDims), _p, ctypes.c_size_t, _p, _p, _p, _p, _p, _p, _p, _p,
+                                  ctypes.c_size_t, _p], _i32),
         "fd_timer_arm": ([_i32, _i32], _i32),
         "fd_timer_read": ([_p, _i32], _i32),
         "fd_timer_disarm": ([], None),
@@ -100,7 +104,8 @@ def lib() -> ctypes.CDLL:
 def exported_symbols() -> Sequence[str]:
     return ("fd_last_error", "fd_version", "fd_plan_build", "fd_region_score_ws_size", "fd_region_score",
             "fd_select", "fd_gather", "fd_embed", "fd_adaln", "fd_block_ws_size", "fd_block_forward", "fd_final",
-            "fd_scatter_update", "fd_timer_arm", "fd_timer_read", "fd_timer_disarm")
+            "fd_scatter_update", "fd_importance_ws_size", "fd_region_importance", "fd_timer_arm", "fd_timer_read",
+            "fd_timer_disarm")
 
 
 def _check(name: str, status: int) -> None:
@@ -250,6 +255,18 @@ def fd_scatter_update(plan: Plan, C: int, x, v, idx, m, dt, vcache, active, skip
                                                         skip_mode, _stream(stream)))
 
 
+def fd_importance_ws_size(plan: Plan, d: FdDims) -> int:
+    return int(lib().fd_importance_ws_size(ctypes.byref(plan.c), ctypes.byref(d)))
+
+
+def fd_region_importance(plan: Plan, d: FdDims, block_ws, k_cache, idx, m, active, r_bar, delta, importance, ws,
+                         stream=None) -> None:
+    _check("fd_region_importance", lib().fd_region_importance(
+        ctypes.byref(plan.c), ctypes.byref(d), _ptr(block_ws), block_ws.numel() * block_ws.element_size(),
+        _ptr(k_cache), _ptr(idx), _ptr(m), _ptr(active), _ptr(r_bar), _ptr(delta), _ptr(importance), _ptr(ws),
+        ws.numel() * ws.element_size(), _stream(stream)))
+
+
 def fd_timer_arm(kernel: str, capacity: int) -> None:
     _check("fd_timer_arm", lib().fd_timer_arm(KERNELS[kernel], capacity))
 
@@ -273,7 +290,9 @@ class SparseStep:
     per-block K/V caches, the gate state and the row workspaces; `step()` issues
     fd_region_score, fd_select, fd_gather, fd_embed, fd_adaln (the modulation of
     all L blocks in one pass), L x fd_block_forward, fd_final and
-    fd_scatter_update on the current stream.
+    fd_scatter_update on the current stream.  With the importance signal the
+    gate thresholds `delta` (carried from the previous step) instead of the
+    region score, and fd_region_importance runs after the chosen block.
     """
 
     def __init__(self, plan: Plan, d: FdDims, params: Dict[str, torch.Tensor], n_layers: int,
@@ -303,23 +322,36 @@ class SparseStep:
         self.mod = torch.zeros((n_layers, B, 6 * D), dtype=torch.float32, device=dev)
         self.block_w = [block_weights(params, l, self.mod[l]) for l in range(n_layers)]
         self.final_w = final_weights(params)
+        self.r_bar = torch.zeros(R, dtype=torch.float64, device=dev)
+        self.delta = torch.zeros(R, dtype=torch.float64, device=dev)
+        self.importance = torch.zeros(R, dtype=torch.float64, device=dev)
+        self.ws_imp = torch.empty(max(fd_importance_ws_size(plan, d), 256), dtype=torch.uint8, device=dev)
 
     def reset_gate(self) -> None:
         self.s_tilde.zero_()
         self.skip_run.zero_()
         self.active.fill_(1)
+        self.r_bar.zero_()
+        self.delta.zero_()
 
     def step(self, x: torch.Tensor, x_prev: torch.Tensor, eps: torch.Tensor, dt: torch.Tensor,
              cond: torch.Tensor, eta: float = 0.0, max_skip: int = 0, skip_mode: int = FD_SKIP_FREEZE,
-             stateless: bool = False, stream=None) -> None:
+             stateless: bool = False, stream=None, signal: str = "delta",
+             importance_block: Optional[int] = None) -> None:
         """One step on the latent x (updated in place); eps fp64 [B], dt fp32 [B], cond fp32 [B, D].
 
         stateless=True gates on fresh scores only (every region counts as
-        executed at the previous step)."""
+        executed at the previous step).  signal="importance" gates on `delta`;
+        importance_block (a block index) updates r_bar and delta from that
+        block's self-attention for the next step."""
         p, d, C = self.plan, self.d, self.d.C
         prev = self.all_active if stateless else self.active
-        fd_region_score(p, C, x, x_prev, self.score, self.ws_score, stream)
-        fd_select(p, self.score, eps, eta, max_skip, self.s_tilde, self.skip_run, prev, self.active,
+        if signal == "importance":
+            score = self.delta
+        else:
+            fd_region_score(p, C, x, x_prev, self.score, self.ws_score, stream)
+            score = self.score
+        fd_select(p, score, eps, eta, max_skip, self.s_tilde, self.skip_run, prev, self.active,
                   self.idx, self.cu_q, self.m, stream)
         fd_gather(p, C, x, self.idx, self.m, self.xa, stream)
         fd_embed(p, d, self.xa, self.params["w_e"], self.params["b_e"], self.params["pos"], self.idx, self.m,
@@ -329,5 +361,8 @@ class SparseStep:
         for l in range(self.L):
             fd_block_forward(p, d, self.block_w[l], cond, self.h, self.idx, self.cu_q, self.m, self.k_cache[l],
                              self.v_cache[l], self.ws_block, stream)
+            if importance_block == l:
+                fd_region_importance(p, d, self.ws_block, self.k_cache[l], self.idx, self.m, self.active, self.r_bar,
+                                     self.delta, self.importance, self.ws_imp, stream)
         fd_final(p, d, self.final_w, cond, self.h, self.cu_q, self.m, self.v, self.ws_block, stream)
         fd_scatter_update(p, C, x, self.v, self.idx, self.m, dt, self.vcache, self.active, skip_mode, stream)

@@ -63,7 +63,8 @@ def make_case(name: str, L: Optional[int] = None, step: int = 0, workload: Optio
 
 
 def run_gpu(case: Case, eps: np.ndarray, x_cur: np.ndarray, x_prev: np.ndarray, eta: float = 0.0,
-            max_skip: int = 0, skip_mode: int = fdl.FD_SKIP_FREEZE, state: Optional[fdl.SparseStep] = None):
+            max_skip: int = 0, skip_mode: int = fdl.FD_SKIP_FREEZE, state: Optional[fdl.SparseStep] = None,
+            signal: str = "delta", importance_block: Optional[int] = None):
     """One step through the C ABI; returns host copies of every output and the step object."""
     w = case.w
     st = state
@@ -75,10 +76,12 @@ def run_gpu(case: Case, eps: np.ndarray, x_cur: np.ndarray, x_prev: np.ndarray, 
     xp = torch.from_numpy(np.ascontiguousarray(x_prev)).cuda()
     st.step(x, xp, torch.from_numpy(np.asarray(eps, np.float64)).cuda(),
             torch.from_numpy(wl.dt_per_request(w)).cuda(), case.cond.cuda(), eta=eta, max_skip=max_skip,
-            skip_mode=skip_mode)
+            skip_mode=skip_mode, signal=signal, importance_block=importance_block)
     torch.cuda.synchronize()
     M = int(st.m.item())
     return dict(score=st.score.cpu().numpy(), active=st.active.cpu().numpy().astype(bool),
+                importance=st.importance.cpu().numpy(), r_bar=st.r_bar.cpu().numpy(),
+                delta=st.delta.cpu().numpy(),
                 idx=st.idx[:M].cpu().numpy(), cu_q=st.cu_q.cpu().numpy(), M=M, x=x.cpu().numpy(),
                 vcache=st.vcache.cpu().numpy(), h=st.h[:M].cpu().numpy(), v=st.v[:M].cpu().numpy(),
                 s_tilde=st.s_tilde.cpu().numpy(), skip_run=st.skip_run.cpu().numpy()), st
@@ -92,25 +95,29 @@ def oracle_caches(case: Case) -> (List[np.ndarray], List[np.ndarray]):
 
 def run_oracle(case: Case, eps: np.ndarray, x_cur: np.ndarray, x_prev: np.ndarray, eta: float = 0.0,
                max_skip: int = 0, skip_mode: int = orc.FREEZE, gate: Optional[orc.GateState] = None,
-               caches=None, vcache: Optional[np.ndarray] = None, sample_rows=None):
+               caches=None, vcache: Optional[np.ndarray] = None, sample_rows=None, signal: str = "delta",
+               importance_block: Optional[int] = None, importance_regions=None):
     w = case.w
     p64 = params_f64(case.params)
     kc, vc = caches if caches is not None else oracle_caches(case)
     out = orc.sparse_step(case.layout, p64, w.H, case.cond.numpy().astype(np.float64), x_cur, x_prev,
                           gate or orc.GateState.fresh(w.R), np.asarray(eps, np.float64), eta, max_skip, kc, vc,
                           case.vcache if vcache is None else vcache, wl.dt_per_request(w), skip_mode,
-                          sample_rows=sample_rows)
+                          sample_rows=sample_rows, signal=signal, importance_block=importance_block,
+                          importance_regions=importance_regions)
     out["k_cache"], out["v_cache"] = kc, vc
     return out
 
 
 def compare_step(case: Case, g: dict, o: dict, x_cur: np.ndarray, gpu_state: fdl.SparseStep,
                  k_in: Optional[torch.Tensor] = None, v_in: Optional[torch.Tensor] = None,
-                 skip_mode: int = orc.FREEZE, tol: float = TOL) -> dict:
+                 skip_mode: int = orc.FREEZE, tol: float = TOL, check_score: bool = True) -> dict:
     """Bit-exact checks on the integer/gate outputs and skipped rows; normwise
-    tolerance on the floating-point outputs.  Returns the measured errors."""
+    tolerance on the floating-point outputs.  Returns the measured errors.
+    check_score=False when the gate ran on a signal other than the region score."""
     w = case.w
-    np.testing.assert_allclose(g["score"], o["score"], rtol=1e-12, atol=0)
+    if check_score:
+        np.testing.assert_allclose(g["score"], o["score"], rtol=1e-12, atol=0)
     np.testing.assert_array_equal(g["active"], o["active"])
     np.testing.assert_array_equal(g["idx"], o["idx"])
     np.testing.assert_array_equal(g["cu_q"], o["cu_q"])

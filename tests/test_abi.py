@@ -106,7 +106,7 @@ def test_block_workspace_size_formula():
     plan = fdl.FdPlan(4096, 64, 1, 64, 4096, *([0x1000] * 6))
     d = fdl.FdDims(64, 1536, 24, 64, 6144)
     got = fdl.lib().fd_block_ws_size(ctypes.byref(plan), ctypes.byref(d))
-    rows = 6 * 1536 * 4 + 3 * 4096 * 1536 * 2 + 4096 * 6144 * 2
+    rows = 6 * 1536 * 4 + 3 * 4096 * 1536 * 2 + 4096 * 6144 * 2 + 4096 * 24 * 4   # ... + per-query normalisers
     # plus split-K scratch: up to 4 fp32 output tiles (at most 256x256) per CU, and their counters
     cus = 256
     assert rows + 4 * cus * (128 * 128 * 4 + 4) <= got <= rows + 4 * cus * (256 * 256 * 4 + 4) + 8 * 256
@@ -127,3 +127,26 @@ def test_adaln_validates_before_launch():
     assert lib.fd_block_forward(ctypes.byref(plan), ctypes.byref(d), ctypes.byref(w), *small) == 2   # ws too small
     w0 = fdl.FdBlockWeights(*([0x1000] * 8 + [0, 0, 0]))
     assert lib.fd_block_forward(ctypes.byref(plan), ctypes.byref(d), ctypes.byref(w0), *small) == 1   # no modulation
+
+
+def test_importance_validates_before_launch():
+    lib = fdl.lib()
+    plan = _fake_plan()
+    d = fdl.FdDims(64, 128, 2, 64, 256)
+    bws = lib.fd_block_ws_size(ctypes.byref(plan), ctypes.byref(d))
+    iws = lib.fd_importance_ws_size(ctypes.byref(plan), ctypes.byref(d))
+    assert iws >= plan.n_tokens * 4 + plan.n_regions * d.H * 4
+    ok = (0x1000, bws, 0x1000, 0x1000, 0x1000, 0x1000, 0x1000, 0x1000, None, 0x1000, iws, None)
+    # null key cache; block workspace too small; importance workspace too small; misaligned
+    assert lib.fd_region_importance(ctypes.byref(plan), ctypes.byref(d), *((0x1000, bws, None) + ok[3:])) == 1
+    assert lib.fd_region_importance(ctypes.byref(plan), ctypes.byref(d), *((0x1000, bws - 1) + ok[2:])) == 2
+    assert lib.fd_region_importance(ctypes.byref(plan), ctypes.byref(d), *(ok[:10] + (iws - 1, None))) == 2
+    assert lib.fd_region_importance(ctypes.byref(plan), ctypes.byref(d), *((0x1010,) + ok[1:])) == 1
+    # a region whose key rows of one head exceed the LDS staging
+    big = fdl.FdPlan(plan.n_tokens, plan.n_regions, 1, 4096, plan.n_tokens, *([0x1000] * 6))
+    d128 = fdl.FdDims(64, 256, 2, 128, 256)
+    bws = lib.fd_block_ws_size(ctypes.byref(big), ctypes.byref(d128))
+    iws = lib.fd_importance_ws_size(ctypes.byref(big), ctypes.byref(d128))
+    assert lib.fd_region_importance(ctypes.byref(big), ctypes.byref(d128), 0x1000, bws, *([0x1000] * 6), None,
+                                    0x1000, iws, None) == 3
+    assert b"LDS" in lib.fd_last_error()

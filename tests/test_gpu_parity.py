@@ -335,3 +335,84 @@ def test_block_forward_with_precomputed_modulation_is_identical():
         outs.append((h.cpu(), kc.cpu(), vc.cpu()))
     for a, b in zip(*outs):
         assert torch.equal(a, b)
+
+
+# ------------------------------------------------------------------ refinement importance
+
+# (workload, blocks, active regions whose importance the oracle computes or None for all)
+IMP_CASES = [("tiny", 1, None), ("image", 2, None), ("audio", 1, None), ("packed", 1, 12), ("video", 1, 3)]
+
+
+@pytest.mark.parametrize("name,L,nreg", IMP_CASES, ids=[c[0] for c in IMP_CASES])
+def test_region_importance_parity(name, L, nreg):
+    """Importance of the active regions from the last block's self-attention
+    (Sec. 3.2, R_i): within 2e-2 of the oracle's; Rbar and Delta start at 0, so
+    after one step both equal R on the active regions and stay 0 on skipped ones."""
+    case = gh.make_case(name, L=L)
+    inp = case.inp
+    g, st = gh.run_gpu(case, inp.eps, inp.x_cur, inp.x_prev, importance_block=L - 1)
+    act = g["active"]
+    regions = None
+    if nreg is not None:
+        regions = np.random.default_rng(21).choice(np.nonzero(act)[0], nreg, replace=False)
+    rows = None
+    if name in ("packed", "video"):
+        rows = np.array([0, g["M"] - 1])
+    gh.say(f"importance {name}: M={g['M']} regions={'all' if regions is None else list(regions)}")
+    o = gh.run_oracle(case, inp.eps, inp.x_cur, inp.x_prev, sample_rows=rows, importance_block=L - 1,
+                      importance_regions=regions)
+    gh.compare_step(case, g, o, inp.x_cur, st)
+    sel = np.nonzero(act)[0] if regions is None else np.asarray(regions)
+    err = rel_err(g["importance"][sel], o["importance"][sel])
+    gh.say(f"  importance error {err:.2e} over {len(sel)} regions")
+    assert err <= gh.TOL
+    assert np.all(np.isnan(g["importance"][~act]))
+    np.testing.assert_array_equal(g["r_bar"][act], g["importance"][act])
+    np.testing.assert_array_equal(g["delta"][act], np.abs(g["importance"][act]))
+    np.testing.assert_array_equal(g["r_bar"][~act], 0.0)
+    np.testing.assert_array_equal(g["delta"][~act], 0.0)
+
+
+def test_importance_gate_chained():
+    """Two steps gated by the importance signal: the first on a designed Delta (the
+    same input on both sides, so the mask is bit-exact), the second on the Delta
+    each side computed from its own first step, with the threshold placed in the
+    widest gap of the oracle's weights so no decision sits within 5% of it."""
+    case = gh.make_case("audio", L=1)
+    w, inp = case.w, case.inp
+    delta0 = np.random.default_rng(22).uniform(0.5, 1.5, w.R)
+    r_bar0 = np.random.default_rng(23).uniform(0.0, 0.02, w.R)
+    eps1 = np.array([1.0 / w.R])
+    st = fdl.SparseStep(case.plan, case.dims, case.params_gpu, w.L, k_cache=case.k_cache.cuda(),
+                        v_cache=case.v_cache.cuda())
+    st.vcache.copy_(torch.from_numpy(case.vcache))
+    st.delta.copy_(torch.from_numpy(delta0))
+    st.r_bar.copy_(torch.from_numpy(r_bar0))
+    gate = orc.GateState.fresh(w.R)
+    gate.delta, gate.r_bar = delta0.copy(), r_bar0.copy()
+    caches = gh.oracle_caches(case)
+    g1, _ = gh.run_gpu(case, eps1, inp.x_cur, inp.x_prev, state=st, signal="importance", importance_block=0)
+    o1 = gh.run_oracle(case, eps1, inp.x_cur, inp.x_prev, gate=gate, caches=caches, signal="importance",
+                       importance_block=0)
+    gh.compare_step(case, g1, o1, inp.x_cur, st, check_score=False)
+    act1 = o1["active"]
+    assert 0 < act1.sum() < w.R
+    assert rel_err(g1["delta"], o1["gate"].delta) <= gh.TOL
+    np.testing.assert_array_equal(g1["delta"][~act1], delta0[~act1])
+    np.testing.assert_array_equal(g1["r_bar"][~act1], r_bar0[~act1])
+    # second step: threshold in the widest relative gap of the oracle's weights
+    d2 = o1["gate"].delta
+    wts = np.sort(d2 / d2.sum())
+    k = int(np.argmax(wts[1:] / np.maximum(wts[:-1], 1e-300)))
+    eps2 = np.array([np.sqrt(wts[k] * wts[k + 1])])
+    margin = np.abs(d2 / d2.sum() - eps2[0]) / eps2[0]
+    assert margin.min() > 0.05
+    gw = g1["delta"] / g1["delta"].sum()
+    np.testing.assert_array_equal(gw >= eps2[0], d2 / d2.sum() >= eps2[0])
+    x1 = g1["x"]
+    g2, _ = gh.run_gpu(case, eps2, x1, inp.x_cur, state=st, signal="importance", importance_block=0)
+    o2 = gh.run_oracle(case, eps2, o1["x"].astype(np.float32), inp.x_cur, gate=o1["gate"], caches=caches,
+                       vcache=o1["vcache"], signal="importance", importance_block=0)
+    np.testing.assert_array_equal(g2["active"], o2["active"])
+    np.testing.assert_array_equal(g2["idx"], o2["idx"])
+    gh.say(f"importance chained: active {int(act1.sum())} then {int(o2['active'].sum())} of {w.R}")
