@@ -3,8 +3,8 @@
 // ones).  Flash-style with an fp32 online softmax (base-2 exponent); both
 // contractions run on v_mfma_f32_32x32x16_bf16.
 //
-// Work unit = (head, query tile of one request, KV split).  A workgroup of 4
-// waves owns a unit of 128 queries, 32 per wave (the code also supports two
+// Work item = (head, query tile of one request).  A workgroup of 4 waves
+// works on 128 queries at a time, 32 per wave (the code also supports two
 // 32-query groups per wave sharing every K/V fragment read; one group measured
 // faster once the loop is software-pipelined).  Each wave computes
 // S^T = K Q^T (keys x queries), so a lane owns one query column: its running max
@@ -381,7 +381,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ACfg<D
     using I0 = std::integral_constant<int, 0>;
     using I1 = std::integral_constant<int, 1>;
     using IK = std::integral_constant<int, KS>;
-    const bool ragged = (k_beg + kt1 * KB > k_end);   // only the split's last tile can hold keys past the end
+    const bool ragged = (k_beg + kt1 * KB > k_end);   // only the piece's last tile can hold keys past the end
     auto body = [&](int t, SAcc& cur, SAcc& nxt) {
       wait_vm_barrier<AHEAD_WAIT>();
       issue(kt0 + min(t + STAGES - 1, nkt - 1), (t + STAGES - 1) % STAGES);
@@ -663,6 +663,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ACfg<D
 
 namespace fdh {
 
+// Partial slots: two per share of a grid of at most two workgroups per CU.
 size_t attn_scratch_bytes(int dh) {
   const size_t units = static_cast<size_t>(gemm_max_tiles());
   const size_t e = static_cast<size_t>(kMaxQG * (((dh + 31) / 32) * 16 + 2));
