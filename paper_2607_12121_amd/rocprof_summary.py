@@ -18,8 +18,8 @@ and the fraction of the peak follow.
 dispatch) into HBM bytes per launch of one kernel.  Each counter is scaled by
 what it reads for a plain copy kernel of S bytes launched in the same run (the
 copy reads S and writes S bytes), so the figure is in the copy's units.  The
-summary records the sha256 of the kernel's sources; a reader that finds other
-sources treats the figure as stale.
+summary records the sha256 of the kernel's sources (code only: comments and
+layout excluded); a reader that finds other code treats the figure as stale.
 """
 from __future__ import annotations
 
@@ -32,12 +32,20 @@ import sys
 from collections import defaultdict
 
 
+def _code_only(text: str) -> str:
+    """Source text without comments and with whitespace runs collapsed: edits to
+    comments or layout leave the digest (and the counters it vouches for) valid."""
+    text = re.sub(r"/\*.*?\*/", " ", text, flags=re.S)
+    text = re.sub(r"//[^\n]*", " ", text)
+    return " ".join(text.split())
+
+
 def source_digest(paths) -> str:
     h = hashlib.sha256()
     for p in sorted(paths):
         h.update(os.path.basename(p).encode())
-        with open(p, "rb") as f:
-            h.update(f.read())
+        with open(p, encoding="utf-8") as f:
+            h.update(_code_only(f.read()).encode())
     return h.hexdigest()
 
 
