@@ -40,6 +40,9 @@ def parse():
     ap.add_argument("--workload", default=WORKLOAD, help="image (default), video, audio, packed or tiny")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU oracle sample")
     ap.add_argument("--no-hbm", action="store_true", help="skip the streaming-kernel bandwidth figures")
+    ap.add_argument("--trajectory", type=int, default=0, metavar="T",
+                    help="instead of the benchmark: T chained steps per threshold and skip mode, deviation "
+                         "of the final latent from the dense trajectory (prints its own JSON line)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="launch a plain fp32 copy of this many MiB 3 times first (counter calibration)")
     return ap.parse_args()
@@ -242,6 +245,41 @@ def cpu_baseline(w, params_gpu, M_expected: int, budget_s: float):
             "seconds_per_step": t_step}
 
 
+def trajectory_study(torch, fdl, wl, w, rm, params, kc, vc, plan, d, cond, dt, T: int) -> dict:
+    """Chained steps x_{n+1} = x_n + dt v(x_n) from the same start, one dense warm-up
+    step (eps = 0) then T - 1 gated steps (stateful gate, forced reactivation after
+    K = 5 skips), for thresholds eps_b = c / R_b and both skip modes; reports the
+    final latent's normwise distance to the dense trajectory (eps = 0 throughout)
+    and the mean active fraction.  Sec. 3.2 bounds that distance by
+    O(eps * sum_n D_n + gamma)."""
+    inp = wl.step_inputs(w, 0, rmap=rm)
+    regs = np.diff(rm.req_reg_off).astype(np.float64)
+
+    def run(c: float, mode: int):
+        st = fdl.SparseStep(plan, d, params, w.L, k_cache=kc.clone(), v_cache=vc.clone())
+        x = torch.from_numpy(inp.x_cur).cuda()
+        xp = torch.from_numpy(inp.x_prev).cuda()
+        act = []
+        for n in range(T):
+            eps = torch.from_numpy(np.zeros(w.B) if n == 0 else c / regs).cuda()
+            x_old = x.clone()
+            st.step(x, xp, eps, dt, cond, max_skip=5, skip_mode=mode)
+            xp = x_old
+            if n > 0:
+                act.append(int(st.m.item()) / w.N)
+        torch.cuda.synchronize()
+        return x, float(np.mean(act)) if act else 1.0
+
+    x_ref, _ = run(0.0, fdl.FD_SKIP_FREEZE)
+    runs = []
+    for mode, name in ((fdl.FD_SKIP_FREEZE, "freeze"), (fdl.FD_SKIP_REUSE_DRIFT, "reuse_drift")):
+        for c in (0.9, 0.95, 1.0, 1.05, 1.1, 1.2):
+            x, af = run(c, mode)
+            dev = float(torch.linalg.vector_norm(x - x_ref) / torch.linalg.vector_norm(x_ref))
+            runs.append({"mode": name, "eps_times_regions": c, "active_frac": af, "rel_dev": dev})
+    return {"trajectory": {"workload": w.name, "steps": T, "max_skip": 5, "dt": float(dt[0].item()), "runs": runs}}
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -280,6 +318,10 @@ def main():
         expected_m.append(int(inp.hot[rm.token_region].sum()))
     cond = wl.make_cond(w, device="cuda")
     dt = torch.from_numpy(wl.dt_per_request(w)).cuda()
+    if args.trajectory > 0:
+        print(json.dumps(trajectory_study(torch, fdl, wl, w, rm, params, kc, vc, plan, d, cond, dt,
+                                          args.trajectory)), flush=True)
+        return 0
 
     def run(i):
         x, xp, eps = pairs[i % args.pool]
