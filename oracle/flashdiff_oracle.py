@@ -29,6 +29,13 @@ What each function follows:
                     come from the cache (Sec. 4 Backend; Prop. "Stale-KV
                     Perturbation").
   latent_update     eq. sf-update with the Euler step of eq. euler.
+  otsu_split, focus_regions, otsu_partition
+                    Sec. 3.1 (Patch Partitioner, "Recursive Load-Aware Patch
+                    Partitioning"), eq. otsu and the r_f allocation.  Readings:
+                    saliency is an integer map (exact class sums); ties keep the
+                    smallest threshold and the smaller r_f; r_f is kept so no
+                    region is empty; a node without any split (one saliency
+                    value) is cut into chunks of consecutive tokens.
   region_importance, importance_update
                     Sec. 3.2 (Patch Gate, "Adaptive Skipping"): the refinement
                     importance R_i = |A_i|^-2 sum_{u,v in A_i} SA_uv of a patch,
@@ -402,3 +409,73 @@ def sparse_step(layout: Layout, params: Dict[str, np.ndarray], n_heads: int, con
     x_new, vc_new = latent_update(x_cur, v, idx[rows], layout, dt, vcache, active, skip_mode)
     return dict(score=score, active=active, idx=idx, cu_q=cu, h=h, v=v, x=x_new, vcache=vc_new,
                 gate=GateState(s_t, run, active, r_bar, delta), rows=rows, importance=imp)
+
+
+# ------------------------------------------------------------------ patch partitioner (Sec. 3.1)
+
+def otsu_split(values: np.ndarray):
+    """Otsu threshold of integer saliency values (eq. otsu): the theta maximising
+    sigma_B^2 = w_f w_c (mu_f - mu_c)^2 over the focus set {v >= theta} and the
+    context set {v < theta}, theta ranging over the distinct values but the
+    smallest (both sets non-empty).  Class sums are exact integers; sigma_B^2 is
+    evaluated in float64 as w_f * w_c * ((S_f / n_f - S_c / n_c) ** 2) with
+    w = n_class / n.  Ties keep the smallest theta.  Returns (theta, sigma_B^2),
+    or None when all values are equal."""
+    v = np.asarray(values, dtype=np.int64)
+    n = len(v)
+    best = None
+    for theta in np.unique(v)[1:]:
+        f = v >= theta
+        n_f = int(f.sum())
+        n_c = n - n_f
+        s_f = int(v[f].sum())
+        s_c = int(v[~f].sum())
+        wf = n_f / n
+        wc = n_c / n
+        d = s_f / n_f - s_c / n_c
+        sb = wf * wc * (d * d)
+        if best is None or sb > best[1]:
+            best = (int(theta), sb)
+    return best
+
+
+def focus_regions(n_f: int, n_c: int, R: int) -> int:
+    """Regions given to the focus set: argmin_{r in 1..R-1} |r - R n_f / (n_f + n_c)|
+    (ties to the smaller r), kept within [max(1, R - n_c), min(R - 1, n_f)] so
+    that no region is empty."""
+    x = R * n_f / (n_f + n_c)
+    r = int(np.floor(x))
+    if x - r > 0.5:
+        r += 1
+    return int(min(max(r, 1, R - n_c), R - 1, n_f))
+
+
+def otsu_partition(saliency: np.ndarray, R: int) -> np.ndarray:
+    """Recursive load-aware patch partitioning (Sec. 3.1): bisect the tokens by
+    the Otsu threshold of their saliency into focus and context sets, give them
+    r_f and R - r_f of the node's R regions by their token share, and recurse
+    until every node holds one region.  Regions are numbered by ranges: a node
+    owning [first, first + R) gives [first, first + r_f) to its focus set.  A
+    node whose tokens all share one saliency value (no split exists) is cut
+    into R chunks of consecutive token indices, chunk c = floor(rank * R / n).
+    Returns the region of every token."""
+    s = np.asarray(saliency, dtype=np.int64)
+    out = np.full(len(s), -1, dtype=np.int64)
+
+    def rec(toks: np.ndarray, first: int, Rn: int):
+        if Rn == 1:
+            out[toks] = first
+            return
+        sp = otsu_split(s[toks])
+        if sp is None:
+            n = len(toks)
+            for rank, t in enumerate(np.sort(toks)):
+                out[t] = first + rank * Rn // n
+            return
+        f = s[toks] >= sp[0]
+        rf = focus_regions(int(f.sum()), int((~f).sum()), Rn)
+        rec(toks[f], first, rf)
+        rec(toks[~f], first + rf, Rn - rf)
+
+    rec(np.arange(len(s)), 0, R)
+    return out

@@ -506,3 +506,67 @@ def test_importance_signal_drives_the_next_gate():
     np.testing.assert_array_equal(o["gate"].delta[~act], gate.delta[~act])
     np.testing.assert_allclose(o["gate"].r_bar[act], o["importance"][act], rtol=0)
     np.testing.assert_allclose(o["gate"].delta[act], np.abs(o["importance"][act] - 0.01), rtol=0)
+
+
+# ------------------------------------------------------------------ patch partitioner (Sec. 3.1)
+
+def test_otsu_threshold_bruteforce_and_variance_decomposition():
+    """The chosen threshold maximises the between-class variance, computed here as
+    sigma_total^2 - sigma_W^2 from the class variances (eq. var-decomp), over
+    every threshold; the two forms of sigma_B^2 agree."""
+    rng = np.random.default_rng(31)
+    for trial in range(20):
+        v = rng.integers(0, 40 if trial % 2 else 4096, int(rng.integers(2, 60)))
+        sp = orc.otsu_split(v)
+        vals = np.unique(v)
+        if len(vals) == 1:
+            assert sp is None
+            continue
+        tot = np.var(v.astype(np.float64))
+        best_t, best_b = None, -1.0
+        for t in vals[1:]:
+            f, c = v[v >= t].astype(np.float64), v[v < t].astype(np.float64)
+            sw = (len(f) * np.var(f) + len(c) * np.var(c)) / len(v)
+            sb = tot - sw
+            if sb > best_b * (1 + 1e-12) + 1e-300:
+                best_t, best_b = int(t), sb
+        assert sp[0] == best_t
+        assert sp[1] == pytest.approx(best_b, rel=1e-9, abs=1e-9)
+
+
+def test_focus_region_allocation():
+    """r_f = argmin |r - R n_f / n| over 1..R-1, ties to the smaller r, kept so no region is empty."""
+    assert orc.focus_regions(30, 70, 10) == 3
+    assert orc.focus_regions(50, 50, 3) == 1          # 1.5: tie
+    assert orc.focus_regions(64, 36, 3) == 2          # 1.92
+    assert orc.focus_regions(1, 99, 10) == 1          # 0.1 -> at least one
+    assert orc.focus_regions(99, 1, 10) == 9          # 9.9 -> at most R - 1
+    assert orc.focus_regions(2, 8, 6) == 1            # 1.2
+    assert orc.focus_regions(2, 3, 5) == 2            # x = 2; context of 3 needs r_f >= 2
+
+
+def test_otsu_partition_two_level_and_constant_maps():
+    """Two saliency levels in two blocks: R = 2 separates them exactly; one level:
+    R chunks of consecutive tokens; R = 1: a single region."""
+    s = np.array([5] * 7 + [900] * 5 + [5] * 3)
+    np.testing.assert_array_equal(orc.otsu_partition(s, 2), np.where(s == 900, 0, 1))
+    np.testing.assert_array_equal(orc.otsu_partition(s, 1), np.zeros(15, np.int64))
+    c = np.full(10, 17)
+    np.testing.assert_array_equal(orc.otsu_partition(c, 3), [0, 0, 0, 0, 1, 1, 1, 2, 2, 2])
+
+
+def test_otsu_partition_invariants():
+    """Exactly R non-empty regions; the root split puts every token of the focus
+    regions above every token of the context regions."""
+    rng = np.random.default_rng(32)
+    for trial in range(6):
+        n = int(rng.integers(40, 400))
+        R = int(rng.integers(2, min(n, 40)))
+        s = rng.integers(0, 4096, n)
+        reg = orc.otsu_partition(s, R)
+        assert reg.min() == 0 and reg.max() == R - 1
+        assert np.all(np.bincount(reg, minlength=R) > 0)
+        theta = orc.otsu_split(s)[0]
+        f = s >= theta
+        rf = orc.focus_regions(int(f.sum()), int((~f).sum()), R)
+        np.testing.assert_array_equal(reg < rf, f)
