@@ -84,6 +84,32 @@ def importance_cost(fdl, stp, run, w, M: int, i: int) -> dict:
             "achieved_tflops": flops / (us * 1e-6) / 1e12 if us > 0 else None}
 
 
+def partition_cost(torch, fdl, wl) -> dict:
+    """Untimed: the patch partitioner, which runs once per request after the
+    warm-up steps, on the workloads' synthetic saliency maps (every request of
+    the batch in one call), each call bracketed by the library's event timer."""
+    out = {"when": "once per request after the warm-up steps (not in the timed step)"}
+    for name in ("image", "audio", "video", "packed"):
+        w = wl.WORKLOADS[name]
+        rm = wl.region_map(w)
+        reg_off = np.concatenate([[0], np.cumsum([rq.n_regions for rq in w.requests])]).astype(np.int32)
+        sal = torch.from_numpy(wl.saliency_maps(w).view(np.int16)).cuda()
+        region = torch.empty(w.N, dtype=torch.int32, device="cuda")
+        ws = torch.empty(max(fdl.fd_partition_ws_size(w.N, w.B), 256), dtype=torch.uint8, device="cuda")
+        for _ in range(3):
+            fdl.fd_partition(rm.req_tok_off, reg_off, sal, region, ws)
+        torch.cuda.synchronize()
+        fdl.fd_timer_arm("partition", 16)
+        for _ in range(10):
+            fdl.fd_partition(rm.req_tok_off, reg_off, sal, region, ws)
+        torch.cuda.synchronize()
+        ms = fdl.fd_timer_read(16)
+        fdl.fd_timer_disarm()
+        out[name] = {"requests": w.B, "tokens": w.N, "regions": int(reg_off[-1]),
+                     "us": round(float(np.mean(ms)) * 1e3, 2)}
+    return out
+
+
 def kernel_bytes(name: str, w, M: int) -> float:
     """Algorithmic HBM bytes of one launch of a streaming kernel."""
     C, N = w.C, w.N
@@ -333,7 +359,7 @@ def main():
 
     # per-kernel time per step (untimed calibration pass, one kernel type at a time)
     per_kernel = {}
-    for name in (k for k in fdl.KERNELS if k != "importance"):
+    for name in (k for k in fdl.KERNELS if k not in ("importance", "partition")):
         fdl.fd_timer_arm(name, 4 * w.L + 8)
         run(0)
         torch.cuda.synchronize()
@@ -383,6 +409,7 @@ def main():
         "kernels_ms_per_step": {k: round(v[0], 4) for k, v in per_kernel.items()},
     }
     out["importance"] = importance_cost(fdl, stp, run, w, M, args.warmup + args.steps)
+    out["partition"] = partition_cost(torch, fdl, wl)
     if not args.no_hbm:
         print("[bench] streaming-kernel bandwidth (score, gather, scatter)", file=sys.stderr, flush=True)
         out["hbm"] = hbm_streams(torch, fdl, wl)

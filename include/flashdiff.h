@@ -16,6 +16,10 @@
  *   fd_final          -> velocity rows
  *   fd_scatter_update -> Euler update of the latent          (eq. sf-update)
  *
+ * Regions come from fd_partition, run once per request on its saliency map
+ * after the warm-up steps (Sec. 3.1): its token->region map is what
+ * fd_plan_build takes.
+ *
  * With the paper's own gate signal, fd_region_importance runs after the block
  * chosen to supply the self-attention, and its Delta replaces the region score
  * at the next step's fd_select (Sec. 3.2, refinement importance).
@@ -260,6 +264,40 @@ fd_status fd_region_importance(const fd_plan* plan, const fd_dims* dims, const v
                                const int32_t* m, const uint8_t* active, double* r_bar, double* delta,
                                double* importance, void* ws, size_t ws_bytes, fd_stream_t stream);
 
+/* ---------------------------------------------------------------- partition
+ * Recursive load-aware patch partitioning (Sec. 3.1, Patch Partitioner; the
+ * between-class variance of eq. otsu; the r_f allocation rule), run once per
+ * request after the warm-up steps, before fd_plan_build.  For every request b
+ * with n_b tokens and R_b regions, a node (initially all tokens, regions
+ * [0, R_b)) is split into focus = {saliency >= theta} and context = the rest,
+ * theta the distinct saliency value (all but the smallest) maximising
+ *   sigma_B^2 = w_f w_c (mu_f - mu_c)^2,  w = class count / node count,
+ * evaluated in fp64 from exact integer class counts and sums as
+ * w_f * w_c * ((S_f / n_f - S_c / n_c)^2), ties to the smaller theta.  The focus
+ * set gets the first r_f of the node's R regions, r_f the r in 1 .. R-1 nearest
+ * to R n_f / (n_f + n_c) (ties to the smaller), clamped to
+ * [max(1, R - n_c), min(R - 1, n_f)]; the context set gets the other R - r_f.
+ * Nodes are split until each holds one region.  A node whose tokens share one
+ * saliency value is cut into its R regions by token index: the token of rank k
+ * (in index order) among its n tokens gets region first + floor(k R / n).
+ *   n_requests   1 .. 64 requests per call
+ *   req_tok_off  host int32 [B+1]  request token ranges, req_tok_off[0] = 0
+ *   req_reg_off  host int32 [B+1]  request region ranges, req_reg_off[0] = 0
+ *   saliency     device uint16 [N] integer saliency of every token (the
+ *                request's quantised saliency map, any 16-bit values)
+ *   token_region device int32 [N]  output: global region id of every token,
+ *                req_reg_off[b] <= id < req_reg_off[b+1] for request b; the
+ *                token_region input of fd_plan_build
+ *   ws           device scratch of fd_partition_ws_size(N, B) bytes, 256-byte aligned
+ * Requirements: 1 <= R_b <= n_b for every request (FD_E_ARG otherwise);
+ * n_b <= 65535 and R_b <= 1024 (FD_E_UNSUPPORTED otherwise).  One workgroup
+ * per request runs the whole recursion in one launch.
+ */
+size_t fd_partition_ws_size(int32_t n_tokens, int32_t n_requests);
+fd_status fd_partition(int32_t n_requests, const int32_t* req_tok_off, const int32_t* req_reg_off,
+                       const uint16_t* saliency, int32_t* token_region, void* ws, size_t ws_bytes,
+                       fd_stream_t stream);
+
 /* ---------------------------------------------------------------- final
  * v[i] = (LN(h_i) * (1 + scale) + shift) W_out^T + b_out, (shift, scale) =
  * SiLU(cond_b) W_ada^T + b_ada, for i < *m.  v device fp32 [N][C].
@@ -293,7 +331,7 @@ fd_status fd_scatter_update(const fd_plan* plan, int32_t C, float* x, const floa
 enum {
   FD_K_SCORE = 1, FD_K_SELECT, FD_K_GATHER, FD_K_EMBED, FD_K_ADALN, FD_K_LN,
   FD_K_GEMM_QKV, FD_K_ATTN, FD_K_GEMM_O, FD_K_GEMM_MLP1, FD_K_GEMM_MLP2,
-  FD_K_FINAL, FD_K_SCATTER, FD_K_IMPORTANCE
+  FD_K_FINAL, FD_K_SCATTER, FD_K_IMPORTANCE, FD_K_PARTITION
 };
 fd_status fd_timer_arm(int32_t kernel, int32_t capacity);
 int32_t fd_timer_read(float* ms, int32_t capacity);

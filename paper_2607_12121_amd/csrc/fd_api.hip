@@ -390,6 +390,37 @@ fd_status fd_region_importance(const fd_plan* plan, const fd_dims* dims, const v
   return FD_OK;
 }
 
+size_t fd_partition_ws_size(int32_t n_tokens, int32_t n_requests) {
+  if (n_tokens < 0 || n_requests < 1) return 0;
+  return fdh::partition_ws_bytes(n_tokens, n_requests);
+}
+
+fd_status fd_partition(int32_t n_requests, const int32_t* req_tok_off, const int32_t* req_reg_off,
+                       const uint16_t* saliency, int32_t* token_region, void* ws, size_t ws_bytes,
+                       fd_stream_t stream) {
+  FD_REQUIRE(req_tok_off && req_reg_off && saliency && token_region && ws, "null pointer");
+  FD_REQUIRE(n_requests >= 1, "n_requests = %d", n_requests);
+  if (n_requests > fd::kMaxPartRequests)
+    return fdh::set_error("%d requests exceed the partitioner's %d per call", n_requests, fd::kMaxPartRequests),
+           FD_E_UNSUPPORTED;
+  FD_REQUIRE(req_tok_off[0] == 0 && req_reg_off[0] == 0, "offsets must start at 0");
+  for (int b = 0; b < n_requests; ++b) {
+    const int n = req_tok_off[b + 1] - req_tok_off[b], r = req_reg_off[b + 1] - req_reg_off[b];
+    FD_REQUIRE(r >= 1 && n >= r, "request %d: %d tokens cannot fill %d regions", b, n, r);
+    if (n > fd::kMaxPartTokens || r > fd::kMaxPartRegions)
+      return fdh::set_error("request %d: %d tokens / %d regions exceed the partitioner's %d / %d", b, n, r,
+                            fd::kMaxPartTokens, fd::kMaxPartRegions),
+             FD_E_UNSUPPORTED;
+  }
+  FD_REQUIRE(aligned(ws, kAlign), "misaligned buffer");
+  const size_t need = fdh::partition_ws_bytes(req_tok_off[n_requests], n_requests);
+  if (ws_bytes < need) return fdh::set_error("partition workspace too small (%zu < %zu)", ws_bytes, need), FD_E_SHAPE;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  FD_LAUNCH(FD_K_PARTITION, s,
+            fdh::launch_partition(n_requests, req_tok_off, req_reg_off, saliency, token_region, ws, s));
+  return FD_OK;
+}
+
 fd_status fd_final(const fd_plan* plan, const fd_dims* dims, const fd_final_weights* w, const float* cond,
                    const float* h, const int32_t* cu_q, const int32_t* m, float* v, void* ws, size_t ws_bytes,
                    fd_stream_t stream) {
@@ -427,7 +458,7 @@ fd_status fd_scatter_update(const fd_plan* plan, int32_t C, float* x, const floa
 }
 
 fd_status fd_timer_arm(int32_t kernel, int32_t capacity) {
-  FD_REQUIRE(kernel >= FD_K_SCORE && kernel <= FD_K_IMPORTANCE && capacity >= 1 && capacity <= (1 << 20),
+  FD_REQUIRE(kernel >= FD_K_SCORE && kernel <= FD_K_PARTITION && capacity >= 1 && capacity <= (1 << 20),
              "bad timer arguments");
   std::lock_guard<std::mutex> lk(g_timer.mu);
   for (hipEvent_t e : g_timer.ev) (void)hipEventDestroy(e);

@@ -16,6 +16,12 @@ namespace fd {
 
 constexpr int kWave = 64;
 
+// Patch partitioner limits: requests per call, regions and tokens per request
+// (per-request counts stay below 2^16 so that two value counts share a word).
+constexpr int kMaxPartRequests = 64;
+constexpr int kMaxPartRegions = 1024;
+constexpr int kMaxPartTokens = 65535;
+
 // fp32 -> bf16 bits, round to nearest even (hardware conversion on gfx950).
 FD_DEVICE uint16_t f2bf(float x) { return __builtin_bit_cast(uint16_t, static_cast<__bf16>(x)); }
 FD_DEVICE float bf2f(uint16_t b) { return __uint_as_float(static_cast<uint32_t>(b) << 16); }
@@ -133,6 +139,11 @@ hipError_t launch_importance(const fd_plan* p, int D, int H, int dh, const int32
                              const uint8_t* active, const uint16_t* q, const uint16_t* kc, const float* lse,
                              int32_t* pos, float* part, double* r_bar, double* delta, double* importance,
                              hipStream_t s);
+
+// Patch partitioner: workspace bytes and the one-launch recursion (offsets are host arrays).
+size_t partition_ws_bytes(int n_tokens, int n_requests);
+hipError_t launch_partition(int n_requests, const int32_t* req_tok_off, const int32_t* req_reg_off,
+                            const uint16_t* saliency, int32_t* region, void* ws, hipStream_t s);
 
 // Bytes of KV-split scratch the attention kernel needs for head dim dh.
 size_t attn_scratch_bytes(int dh);

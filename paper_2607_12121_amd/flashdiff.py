@@ -24,7 +24,7 @@ FD_SKIP_REUSE_DRIFT = 1
 
 KERNELS = {"score": 1, "select": 2, "gather": 3, "embed": 4, "adaln": 5, "ln": 6, "gemm_qkv": 7,
            "attn": 8, "gemm_o": 9, "gemm_mlp1": 10, "gemm_mlp2": 11, "final": 12, "scatter": 13,
-           "importance": 14}
+           "importance": 14, "partition": 15}
 
 _p = ctypes.c_void_p
 _i32 = ctypes.c_int32
@@ -89,6 +89,8 @@ def lib() -> ctypes.CDLL:
         "fd_importance_ws_size": ([P(FdPlan), P(FdDims)], ctypes.c_size_t),
         "fd_region_importance": ([P(FdPlan), P(FdDims), _p, ctypes.c_size_t, _p, _p, _p, _p, _p, _p, _p, _p,
                                   ctypes.c_size_t, _p], _i32),
+        "fd_partition_ws_size": ([_i32, _i32], ctypes.c_size_t),
+        "fd_partition": ([_i32, _p, _p, _p, _p, _p, ctypes.c_size_t, _p], _i32),
         "fd_timer_arm": ([_i32, _i32], _i32),
         "fd_timer_read": ([_p, _i32], _i32),
         "fd_timer_disarm": ([], None),
@@ -104,8 +106,8 @@ def lib() -> ctypes.CDLL:
 def exported_symbols() -> Sequence[str]:
     return ("fd_last_error", "fd_version", "fd_plan_build", "fd_region_score_ws_size", "fd_region_score",
             "fd_select", "fd_gather", "fd_embed", "fd_adaln", "fd_block_ws_size", "fd_block_forward", "fd_final",
-            "fd_scatter_update", "fd_importance_ws_size", "fd_region_importance", "fd_timer_arm", "fd_timer_read",
-            "fd_timer_disarm")
+            "fd_scatter_update", "fd_importance_ws_size", "fd_region_importance", "fd_partition_ws_size",
+            "fd_partition", "fd_timer_arm", "fd_timer_read", "fd_timer_disarm")
 
 
 def _check(name: str, status: int) -> None:
@@ -265,6 +267,35 @@ def fd_region_importance(plan: Plan, d: FdDims, block_ws, k_cache, idx, m, activ
         ctypes.byref(plan.c), ctypes.byref(d), _ptr(block_ws), block_ws.numel() * block_ws.element_size(),
         _ptr(k_cache), _ptr(idx), _ptr(m), _ptr(active), _ptr(r_bar), _ptr(delta), _ptr(importance), _ptr(ws),
         ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def fd_partition_ws_size(n_tokens: int, n_requests: int) -> int:
+    return int(lib().fd_partition_ws_size(n_tokens, n_requests))
+
+
+def fd_partition(req_tok_off, req_reg_off, saliency, token_region, ws, stream=None) -> None:
+    """Patch partitioner.  req_tok_off, req_reg_off: host int sequences [B+1];
+    saliency: device 2-byte tensor [N] holding uint16 values; token_region:
+    device int32 [N] (output); ws: device bytes of fd_partition_ws_size(N, B)."""
+    to = np.ascontiguousarray(req_tok_off, dtype=np.int32)
+    ro = np.ascontiguousarray(req_reg_off, dtype=np.int32)
+    if to.shape != ro.shape or to.ndim != 1 or len(to) < 2:
+        raise FlashDiffError("req_tok_off and req_reg_off must both have B + 1 entries")
+    if saliency.element_size() != 2 or token_region.dtype != torch.int32:
+        raise FlashDiffError("saliency must hold 16-bit values and token_region int32")
+    _check("fd_partition", lib().fd_partition(len(to) - 1, to.ctypes.data, ro.ctypes.data, _ptr(saliency),
+                                              _ptr(token_region), _ptr(ws), ws.numel() * ws.element_size(),
+                                              _stream(stream)))
+
+
+def partition(saliency: torch.Tensor, req_tok_off, req_reg_off, stream=None) -> torch.Tensor:
+    """fd_partition with its output and workspace allocated here: the global
+    region id of every token (device int32 [N])."""
+    N, B = int(saliency.numel()), len(req_tok_off) - 1
+    out = torch.empty(N, dtype=torch.int32, device=saliency.device)
+    ws = torch.empty(max(fd_partition_ws_size(N, B), 256), dtype=torch.uint8, device=saliency.device)
+    fd_partition(req_tok_off, req_reg_off, saliency, out, ws, stream)
+    return out
 
 
 def fd_timer_arm(kernel: str, capacity: int) -> None:

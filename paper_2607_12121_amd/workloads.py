@@ -327,3 +327,31 @@ def make_kv_cache(w: Workload, seed: int = 99, device: str = "cpu", layers: Opti
 
 def dt_per_request(w: Workload) -> np.ndarray:
     return np.full(w.B, w.dt, dtype=np.float32)
+
+
+def saliency_map(shape: RequestShape, seed: int, levels: int = 4096) -> np.ndarray:
+    """Synthetic saliency map of one request (uint16 [n_tokens], values in
+    [0, levels)): a stand-in for the cross-attention of the prompt's salient
+    tokens averaged over those tokens, which concentrates on a few objects of
+    the latent.  Recipe: K ~ U{3, ..., 6} Gaussian blobs over the request's
+    grid in normalised coordinates (each axis in [0, 1]), centres uniform,
+    per-axis widths U[0.05, 0.25], amplitudes U[0.3, 1], plus a background
+    U[0, 0.05] per token; the field is scaled so that its maximum maps to
+    levels - 1 and rounded down (a quantised map)."""
+    rng = np.random.default_rng(seed)
+    coords = np.indices(shape.dims).reshape(len(shape.dims), -1).astype(np.float64)
+    coords /= np.maximum(np.array(shape.dims, dtype=np.float64) - 1.0, 1.0)[:, None]
+    field = rng.uniform(0.0, 0.05, coords.shape[1])
+    for _ in range(int(rng.integers(3, 7))):
+        centre = rng.uniform(0.0, 1.0, (len(shape.dims), 1))
+        width = rng.uniform(0.05, 0.25, (len(shape.dims), 1))
+        field += rng.uniform(0.3, 1.0) * np.exp(-0.5 * (((coords - centre) / width) ** 2).sum(axis=0))
+    q = np.floor(field / field.max() * (levels - 1))
+    return np.clip(q, 0, levels - 1).astype(np.uint16)
+
+
+def saliency_maps(w: Workload, seed: Optional[int] = None, levels: int = 4096) -> np.ndarray:
+    """saliency_map of every request of the workload, concatenated in request
+    order (uint16 [N]); request b uses seed + b."""
+    s = w.seed + 7 if seed is None else seed
+    return np.concatenate([saliency_map(rq, s + b, levels) for b, rq in enumerate(w.requests)])

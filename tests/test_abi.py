@@ -150,3 +150,31 @@ def test_importance_validates_before_launch():
     assert lib.fd_region_importance(ctypes.byref(big), ctypes.byref(d128), 0x1000, bws, *([0x1000] * 6), None,
                                     0x1000, iws, None) == 3
     assert b"LDS" in lib.fd_last_error()
+
+
+def test_partition_validates_before_launch():
+    lib = fdl.lib()
+    to = np.array([0, 100, 300], np.int32)
+    ro = np.array([0, 8, 24], np.int32)
+    need = lib.fd_partition_ws_size(300, 2)
+    assert need >= 2 * 300 * 4 + 302 * 12
+    assert lib.fd_partition_ws_size(300, 0) == 0
+
+    def call(t, r, B=2, ws=0x1000, nbytes=need, sal=0x1000):
+        t = np.ascontiguousarray(t, np.int32)
+        r = np.ascontiguousarray(r, np.int32)
+        return lib.fd_partition(B, t.ctypes.data, r.ctypes.data, sal, 0x1000, ws, nbytes, None)
+
+    assert call(to, ro, sal=None) == 1                          # null saliency
+    assert call(to, ro, B=0) == 1                               # no request
+    assert call([1, 100, 300], ro) == 1                         # offsets not from 0
+    assert call(to, [0, 8, 8]) == 1                             # request without regions
+    assert call([0, 5, 300], ro) == 1                           # 5 tokens cannot fill 8 regions
+    assert b"cannot fill" in lib.fd_last_error()
+    assert call(to, ro, ws=0x1010) == 1                         # misaligned workspace
+    assert call(to, ro, nbytes=need - 1) == 2                   # workspace too small
+    assert call([0, 65536], [0, 8], B=1, nbytes=1 << 30) == 3   # request of 2^16 tokens
+    assert call([0, 4096], [0, 1025], B=1, nbytes=1 << 30) == 3  # 1025 regions
+    many = np.arange(66, dtype=np.int32) * 10
+    assert call(many, many, B=65, nbytes=1 << 30) == 3          # 65 requests in one call
+    assert b"requests" in lib.fd_last_error()
