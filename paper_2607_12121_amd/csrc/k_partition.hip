@@ -15,7 +15,7 @@
 // One workgroup per request runs the whole recursion: the 16-bit value
 // histogram (two bins per LDS word, counts below 2^16), the distinct-value list
 // with its prefix counts and sums (global workspace), one level of splits at a
-// time with one wave per node, and the region of every token.  No host round trip.
+// time with the workgroup's waves shared among the nodes, and the region of every token.  No host round trip.
 #include "fd_common.h"
 
 namespace {
@@ -110,6 +110,8 @@ __global__ __launch_bounds__(kPartThreads) void partition_kernel(const uint16_t*
   __shared__ int s_sx[kPartWaves], s_sy[kPartWaves];
   __shared__ int64_t s_sz[kPartWaves];
   __shared__ int s_ntodo;
+  __shared__ double s_best[kPartWaves];
+  __shared__ int s_bp[kPartWaves];
 
   const int req = blockIdx.x;
   const int T0 = reqs.tok_off[req], n = reqs.tok_off[req + 1] - T0;
@@ -178,8 +180,10 @@ __global__ __launch_bounds__(kPartThreads) void partition_kernel(const uint16_t*
   __syncthreads();
 
   // One level of splits per pass.  A node owns the region ids [f, f + rn[f]) and
-  // only the wave that splits it writes entries inside that range.  Every pass
-  // splits or ends each node it takes, so at most R passes run.
+  // only the thread that splits it writes entries inside that range.  Every
+  // pass splits or ends each node it takes, so at most R passes run.  With K
+  // nodes to split, a group of wpn = 16 / K waves (a power of two, at least 1)
+  // scans each node's candidates; groups take the nodes in rounds.
   for (int level = 0; level <= R; ++level) {
     if (wave == 0) {
       int k = 0;
@@ -195,33 +199,50 @@ __global__ __launch_bounds__(kPartThreads) void partition_kernel(const uint16_t*
     __syncthreads();
     const int K = s_ntodo;
     if (K == 0) break;
-    for (int j = wave; j < K; j += kPartWaves) {
-      const int f = s_todo[j];
-      const int a = s_a[f], b = s_b[f], Rn = s_rn[f];
-      if (b - a == 1) {   // one saliency value: no split
-        if (lane == 0) s_kind[f] = kChunk;
-        continue;
+    int wpn = kPartWaves;
+    while (wpn > 1 && wpn * K > kPartWaves) wpn >>= 1;
+    const int groups = kPartWaves / wpn, sub = wave % wpn, stride = wpn * fd::kWave;
+    for (int j0 = 0; j0 < K; j0 += groups) {
+      const int j = j0 + wave / wpn;
+      int f = 0, a = 0, b = 0;
+      if (j < K) {
+        f = s_todo[j];
+        a = s_a[f];
+        b = s_b[f];
       }
-      const int pa = pc[a];
-      const int64_t sa = ps[a];
-      const int64_t nn = pc[b] - pa, tot = ps[b] - sa;
+      const int pa = j < K ? pc[a] : 0;
+      const int64_t sa = j < K ? ps[a] : 0;
+      const int64_t nn = j < K ? pc[b] - pa : 0, tot = j < K ? ps[b] - sa : 0;
       double best = -1.0;
       int bp = b;
-      {
+      if (j < K) {
 #pragma clang fp contract(off)
         // between-class variance w_f w_c (mu_f - mu_c)^2 of the split at each
-        // distinct value but the smallest, from exact integer counts and sums
-        for (int p = a + 1 + lane; p < b; p += fd::kWave) {
-          const int64_t n_c = pc[p] - pa, s_c = ps[p] - sa;
-          const int64_t n_f = nn - n_c, s_f = tot - s_c;
-          const double wf = static_cast<double>(n_f) / static_cast<double>(nn);
-          const double wc = static_cast<double>(n_c) / static_cast<double>(nn);
-          const double d = static_cast<double>(s_f) / static_cast<double>(n_f) -
-                           static_cast<double>(s_c) / static_cast<double>(n_c);
-          const double sb = wf * wc * (d * d);
-          if (sb > best) {
-            best = sb;
-            bp = p;
+        // distinct value but the smallest, from exact integer counts and sums;
+        // four candidates' prefix loads in flight per lane, ascending order kept
+        for (int p0 = a + 1 + sub * fd::kWave + lane; p0 < b; p0 += 4 * stride) {
+          int64_t ncs[4], scs[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const int p = p0 + u * stride;
+            ncs[u] = p < b ? pc[p] : 0;
+            scs[u] = p < b ? ps[p] : 0;
+          }
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const int p = p0 + u * stride;
+            if (p >= b) continue;
+            const int64_t n_c = ncs[u] - pa, s_c = scs[u] - sa;
+            const int64_t n_f = nn - n_c, s_f = tot - s_c;
+            const double wf = static_cast<double>(n_f) / static_cast<double>(nn);
+            const double wc = static_cast<double>(n_c) / static_cast<double>(nn);
+            const double d = static_cast<double>(s_f) / static_cast<double>(n_f) -
+                             static_cast<double>(s_c) / static_cast<double>(n_c);
+            const double sb = wf * wc * (d * d);
+            if (sb > best) {
+              best = sb;
+              bp = p;
+            }
           }
         }
       }
@@ -235,19 +256,34 @@ __global__ __launch_bounds__(kPartThreads) void partition_kernel(const uint16_t*
         }
       }
       if (lane == 0) {
-        const int64_t n_c = pc[bp] - pa;
-        const int rf = focus_share(nn - n_c, n_c, Rn);
-        s_a[f] = bp;
-        s_b[f] = b;
-        s_rn[f] = rf;
-        s_kind[f] = rf > 1 ? kSplit : kLeaf;
-        s_a[f + rf] = a;
-        s_b[f + rf] = bp;
-        s_rn[f + rf] = Rn - rf;
-        s_kind[f + rf] = Rn - rf > 1 ? kSplit : kLeaf;
+        s_best[wave] = best;
+        s_bp[wave] = bp;
       }
+      __syncthreads();
+      if (j < K && sub == 0 && lane == 0) {
+        const int Rn = s_rn[f];
+        if (b - a == 1) {   // one saliency value: no split
+          s_kind[f] = kChunk;
+        } else {
+          for (int w = wave + 1; w < wave + wpn; ++w)
+            if (s_best[w] > best || (s_best[w] == best && s_bp[w] < bp)) {
+              best = s_best[w];
+              bp = s_bp[w];
+            }
+          const int64_t n_c = pc[bp] - pa;
+          const int rf = focus_share(nn - n_c, n_c, Rn);
+          s_a[f] = bp;
+          s_b[f] = b;
+          s_rn[f] = rf;
+          s_kind[f] = rf > 1 ? kSplit : kLeaf;
+          s_a[f + rf] = a;
+          s_b[f + rf] = bp;
+          s_rn[f + rf] = Rn - rf;
+          s_kind[f + rf] = Rn - rf > 1 ? kSplit : kLeaf;
+        }
+      }
+      __syncthreads();
     }
-    __syncthreads();
   }
 
   // node of every distinct value
