@@ -25,6 +25,11 @@ constexpr int kPartWaves = kPartThreads / fd::kWave;
 constexpr int kValues = 65536;                  // saliency is uint16
 constexpr int kValWords = kValues / 2;          // two 16-bit bins per word
 constexpr int kWordsPerThread = kValWords / kPartThreads;
+// One pad word after every 32: a thread's 32 consecutive words then start 33
+// words after its neighbour's, so a wave's reads of them hit distinct banks.
+constexpr int kBinWords = kValWords + kValWords / 32;
+
+FD_DEVICE int bin_word(int w) { return w + (w >> 5); }
 
 enum : uint8_t { kNone = 0, kSplit = 1, kLeaf = 2, kChunk = 3 };
 
@@ -103,7 +108,7 @@ FD_DEVICE int focus_share(int64_t n_f, int64_t n_c, int R) {
 __global__ __launch_bounds__(kPartThreads) void partition_kernel(const uint16_t* __restrict__ saliency,
                                                                  PartReqs reqs, PartWs ws,
                                                                  int32_t* __restrict__ region) {
-  __shared__ uint32_t s_bins[kValWords];   // value counts, then value -> distinct index
+  __shared__ uint32_t s_bins[kBinWords];   // value counts, then value -> distinct index (padded)
   __shared__ int32_t s_a[fd::kMaxPartRegions], s_b[fd::kMaxPartRegions], s_rn[fd::kMaxPartRegions];
   __shared__ int16_t s_todo[fd::kMaxPartRegions];
   __shared__ uint8_t s_kind[fd::kMaxPartRegions];
@@ -112,6 +117,7 @@ __global__ __launch_bounds__(kPartThreads) void partition_kernel(const uint16_t*
   __shared__ int s_ntodo;
   __shared__ double s_best[kPartWaves];
   __shared__ int s_bp[kPartWaves];
+  __shared__ int64_t s_nc[kPartWaves];
 
   const int req = blockIdx.x;
   const int T0 = reqs.tok_off[req], n = reqs.tok_off[req + 1] - T0;
@@ -124,21 +130,21 @@ __global__ __launch_bounds__(kPartThreads) void partition_kernel(const uint16_t*
   const int tid = threadIdx.x, lane = tid & (fd::kWave - 1), wave = tid / fd::kWave;
 
   // histogram of the request's saliency values
-  for (int w = tid; w < kValWords; w += kPartThreads) s_bins[w] = 0;
+  for (int w = tid; w < kBinWords; w += kPartThreads) s_bins[w] = 0;
   __syncthreads();
   for (int t = tid; t < n; t += kPartThreads) {
     const int v = sal[t];
-    atomicAdd(&s_bins[v >> 1], 1u << ((v & 1) * 16));
+    atomicAdd(&s_bins[bin_word(v >> 1)], 1u << ((v & 1) * 16));
   }
   __syncthreads();
 
   // distinct values in ascending order with exclusive prefix counts and sums;
   // every bin word is replaced by the distinct indices of its two values
-  const int w0 = tid * kWordsPerThread;
+  const int w0 = tid * kWordsPerThread, p0 = bin_word(w0);
   int nz = 0, cnt = 0;
   int64_t sum = 0;
   for (int j = 0; j < kWordsPerThread; ++j) {
-    const uint32_t word = s_bins[w0 + j];
+    const uint32_t word = s_bins[p0 + j];
     const int c0 = static_cast<int>(word & 0xffffu), c1 = static_cast<int>(word >> 16);
     const int v = 2 * (w0 + j);
     nz += (c0 > 0) + (c1 > 0);
@@ -149,7 +155,7 @@ __global__ __launch_bounds__(kPartThreads) void partition_kernel(const uint16_t*
   int64_t s_all;
   block_scan3(nz, cnt, sum, U, n_all, s_all, s_sx, s_sy, s_sz);
   for (int j = 0; j < kWordsPerThread; ++j) {
-    const uint32_t word = s_bins[w0 + j];
+    const uint32_t word = s_bins[p0 + j];
     uint32_t map = 0;
     for (int h = 0; h < 2; ++h) {
       const int c = static_cast<int>((word >> (16 * h)) & 0xffffu);
@@ -163,7 +169,7 @@ __global__ __launch_bounds__(kPartThreads) void partition_kernel(const uint16_t*
       cnt += c;
       sum += static_cast<int64_t>(c) * v;
     }
-    s_bins[w0 + j] = map;
+    s_bins[p0 + j] = map;
   }
   if (tid == 0) {
     pc[U] = n_all;
@@ -215,6 +221,7 @@ __global__ __launch_bounds__(kPartThreads) void partition_kernel(const uint16_t*
       const int64_t nn = j < K ? pc[b] - pa : 0, tot = j < K ? ps[b] - sa : 0;
       double best = -1.0;
       int bp = b;
+      int64_t bnc = 0;   // context count of the best split
       if (j < K) {
 #pragma clang fp contract(off)
         // between-class variance w_f w_c (mu_f - mu_c)^2 of the split at each
@@ -242,6 +249,7 @@ __global__ __launch_bounds__(kPartThreads) void partition_kernel(const uint16_t*
             if (sb > best) {
               best = sb;
               bp = p;
+              bnc = n_c;
             }
           }
         }
@@ -250,14 +258,17 @@ __global__ __launch_bounds__(kPartThreads) void partition_kernel(const uint16_t*
       for (int o = fd::kWave / 2; o > 0; o >>= 1) {
         const double ob = __shfl_xor(best, o, fd::kWave);
         const int op = __shfl_xor(bp, o, fd::kWave);
+        const int64_t onc = __shfl_xor(bnc, o, fd::kWave);
         if (ob > best || (ob == best && op < bp)) {
           best = ob;
           bp = op;
+          bnc = onc;
         }
       }
       if (lane == 0) {
         s_best[wave] = best;
         s_bp[wave] = bp;
+        s_nc[wave] = bnc;
       }
       __syncthreads();
       if (j < K && sub == 0 && lane == 0) {
@@ -269,9 +280,9 @@ __global__ __launch_bounds__(kPartThreads) void partition_kernel(const uint16_t*
             if (s_best[w] > best || (s_best[w] == best && s_bp[w] < bp)) {
               best = s_best[w];
               bp = s_bp[w];
+              bnc = s_nc[w];
             }
-          const int64_t n_c = pc[bp] - pa;
-          const int rf = focus_share(nn - n_c, n_c, Rn);
+          const int rf = focus_share(nn - bnc, bnc, Rn);
           s_a[f] = bp;
           s_b[f] = b;
           s_rn[f] = rf;
@@ -297,7 +308,7 @@ __global__ __launch_bounds__(kPartThreads) void partition_kernel(const uint16_t*
   // tokens of one-region nodes
   for (int t = tid; t < n; t += kPartThreads) {
     const int v = sal[t];
-    const int k = static_cast<int>((s_bins[v >> 1] >> ((v & 1) * 16)) & 0xffffu);
+    const int k = static_cast<int>((s_bins[bin_word(v >> 1)] >> ((v & 1) * 16)) & 0xffffu);
     const int f = node_of[k];
     if (s_kind[f] == kLeaf) region[T0 + t] = G0 + f;
   }
