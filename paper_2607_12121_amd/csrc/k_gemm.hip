@@ -139,7 +139,9 @@ struct TileCfg {
 };
 using CfgSmall = TileCfg<128, 128, 2, 2, 2, 2>;
 using CfgWide = TileCfg<128, 192, 2, 2, 2, 2>;     // 1.5x the columns: one round where 128x128 needs two
-using CfgNarrow = TileCfg<128, 64, 2, 2, 2, 2>;    // half the columns: twice the tiles when few
+// half the columns: twice the tiles when few; its 24 KB stages fit three in the
+// shared ring, and the third stage hides the load latency that two exposed
+using CfgNarrow = TileCfg<128, 64, 2, 2, 3, 2>;
 using CfgLarge = TileCfg<256, 256, 2, 4, 2, 1>;
 constexpr int kSmallTile = 128 * 128;   // split-K partial tile (floats)
 // LDS ring of the two-workgroups-per-CU kernel: the largest of its three tile shapes
@@ -377,8 +379,9 @@ FD_DEVICE void gemm_tiles(const fdh::GemmArgs& g, int slots, int M, uint4* ring_
 // Tile shape of the two-workgroups-per-CU kernel for M rows (identical in every
 // WG): 128x128 whenever split-K applies; otherwise the shape whose rounds of tiles
 // over the resident slots cost least, a round of 128x64 / 128x128 / 128x192 tiles
-// weighted 10 / 13 / 22 (measured per-round times at 1664 rows); ties go to the
-// larger tile.  0 = 128x128, 1 = 128x192, 2 = 128x64.
+// weighted 8 / 13 / 22 (measured per-round times at 1664 rows); ties go to the
+// larger tile.  0 = 128x128, 1 = 128x192, 2 = 128x64 (three-stage ring: a round
+// costs 8 where its two-stage version cost 10).
 FD_DEVICE int small_shape(int M, int N, int K, int slots, int max_units) {
   const int tm = (M + 127) / 128;
   const int t128 = tm * ((N + 127) / 128);
@@ -386,7 +389,7 @@ FD_DEVICE int small_shape(int M, int N, int K, int slots, int max_units) {
   const int r128 = (t128 + slots - 1) / slots;
   const int r192 = (tm * ((N + 191) / 192) + slots - 1) / slots;
   const int r64 = (tm * ((N + 63) / 64) + slots - 1) / slots;
-  const int c128 = 13 * r128, c192 = 22 * r192, c64 = 10 * r64;
+  const int c128 = 13 * r128, c192 = 22 * r192, c64 = 8 * r64;
   if (c192 <= c128 && c192 <= c64) return 1;
   if (c128 <= c64) return 0;
   return 2;
