@@ -570,3 +570,26 @@ def test_otsu_partition_invariants():
         f = s >= theta
         rf = orc.focus_regions(int(f.sum()), int((~f).sum()), R)
         np.testing.assert_array_equal(reg < rf, f)
+
+
+def test_saliency_maps_recipe_and_partition_balance():
+    """The synthetic saliency maps follow their recipe (uint16, maximum at
+    levels - 1, seeded), and the oracle partitions every workload's map into
+    exactly its region count, each region holding at least one token and the
+    focus class of every root split the high-saliency side."""
+    for name in ("tiny", "image", "audio", "packed"):
+        w = wl.WORKLOADS[name]
+        s = wl.saliency_maps(w)
+        assert s.dtype == np.uint16 and s.shape == (w.N,)
+        assert np.array_equal(s, wl.saliency_maps(w))
+        rm = wl.region_map(w)
+        for b, rq in enumerate(w.requests):
+            seg = s[rm.req_tok_off[b]:rm.req_tok_off[b + 1]].astype(np.int64)
+            assert seg.max() == 4095
+            reg = orc.otsu_partition(seg, rq.n_regions)
+            counts = np.bincount(reg, minlength=rq.n_regions)
+            assert len(counts) == rq.n_regions and counts.min() >= 1
+            theta, _ = orc.otsu_split(seg)
+            rf = orc.focus_regions(int((seg >= theta).sum()), int((seg < theta).sum()), rq.n_regions)
+            assert seg[reg < rf].min() >= theta > seg[reg >= rf].max()
+    assert wl.saliency_map(wl.RequestShape("seq", (300,), (30,)), seed=3, levels=256).max() == 255
