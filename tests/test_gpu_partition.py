@@ -62,11 +62,15 @@ def test_partition_workload_maps(name):
 
 
 def test_partition_full_16_bit_range():
-    """Values spanning 0 .. 65535 (class sums beyond 2^32)."""
+    """Values spanning 0 .. 65535 (class sums beyond 2^32); a map of about 14000
+    distinct values (that many candidate thresholds at the root)."""
     shape = wl.RequestShape("grid2d", (64, 64), (8, 8))
     sal = wl.saliency_map(shape, seed=5, levels=65536)
     assert sal.max() == 65535
     _check("16-bit image", sal, [0, 4096], [0, 64])
+    many = np.random.default_rng(6).integers(0, 65536, 16000).astype(np.uint16)
+    assert len(np.unique(many)) > 14000
+    _check("many distinct values", many, [0, 16000], [0, 64])
 
 
 def test_partition_constant_and_few_values():
