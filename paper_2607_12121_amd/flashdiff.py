@@ -295,6 +295,8 @@ def partition(saliency: torch.Tensor, req_tok_off, req_reg_off, stream=None) -> 
     out = torch.empty(N, dtype=torch.int32, device=saliency.device)
     ws = torch.empty(max(fd_partition_ws_size(N, B), 256), dtype=torch.uint8, device=saliency.device)
     fd_partition(req_tok_off, req_reg_off, saliency, out, ws, stream)
+    if stream is not None:   # the workspace is freed here while the kernel may still run on `stream`
+        ws.record_stream(stream)
     return out
 
 
