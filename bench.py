@@ -309,7 +309,7 @@ def trajectory_study(torch, fdl, wl, w, rm, params, kc, vc, plan, d, cond, dt, T
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; use --gpus 1", "n_gpus": args.gpus}))
+        print(json.dumps({"error": "the region-sparse step is implemented for a single GPU; use --gpus 1", "n_gpus": args.gpus}))
         return 2
     import torch
 
