@@ -178,3 +178,17 @@ def test_partition_validates_before_launch():
     many = np.arange(66, dtype=np.int32) * 10
     assert call(many, many, B=65, nbytes=1 << 30) == 3          # 65 requests in one call
     assert b"requests" in lib.fd_last_error()
+
+
+def test_binding_fails_loudly_without_the_library(tmp_path):
+    """No CPU fallback: with the shared library missing, the binding raises on
+    first use (checked in a fresh interpreter, whose loader cache is empty)."""
+    import subprocess
+    import sys
+    code = ("from paper_2607_12121_amd import flashdiff as f\n"
+            "try:\n    f.lib()\nexcept f.FlashDiffError as e:\n    print('raised:', e)\n")
+    env = dict(os.environ, FLASHDIFF_LIB=str(tmp_path / "absent.so"))
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    out = subprocess.run([sys.executable, "-c", code], env=env, cwd=root, capture_output=True, text=True,
+                         timeout=300)
+    assert out.returncode == 0 and "raised:" in out.stdout and "missing" in out.stdout, out.stderr[-2000:]
