@@ -593,3 +593,19 @@ def test_saliency_maps_recipe_and_partition_balance():
             rf = orc.focus_regions(int((seg >= theta).sum()), int((seg < theta).sum()), rq.n_regions)
             assert seg[reg < rf].min() >= theta > seg[reg >= rf].max()
     assert wl.saliency_map(wl.RequestShape("seq", (300,), (30,)), seed=3, levels=256).max() == 255
+
+
+def test_focus_allocation_is_the_constrained_argmin():
+    """r_f equals, by brute force, the argmin of |r - R n_f / (n_f + n_c)| over the
+    r that leave no region empty (max(1, R - n_c) <= r <= min(R - 1, n_f)), ties
+    to the smaller r, computed with exact rationals."""
+    from fractions import Fraction
+    for R in range(2, 13):
+        for n_f in range(1, 16):
+            for n_c in range(1, 16):
+                lo, hi = max(1, R - n_c), min(R - 1, n_f)
+                if lo > hi:
+                    continue
+                x = Fraction(R * n_f, n_f + n_c)
+                want = min(range(lo, hi + 1), key=lambda r: (abs(r - x), r))
+                assert orc.focus_regions(n_f, n_c, R) == want, (n_f, n_c, R)
