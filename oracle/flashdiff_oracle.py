@@ -58,6 +58,13 @@ from typing import Dict, List, Optional
 import numpy as np
 
 LN_EPS = 1e-6
+# Tie band of the gate comparison.  The paper's weights are real numbers and a
+# region whose weight equals eps is active; binary64 cannot decide such a tie
+# exactly (D_b = sum of fl(s~ + eta) over up to 4096 regions carries a relative
+# rounding error below 4097 * 2^-53 < 2^-40), so a region counts as below the
+# threshold only when fl(s~ + eta) < fl(eps * D_b) * (1 - 2^-40).  Every
+# exact-arithmetic tie is then active, whatever way D_b rounds.
+TIE_BAND = 2.0 ** -40
 FREEZE = 0          # skipped latent rows are left unchanged
 REUSE_DRIFT = 1     # skipped latent rows advance with their cached drift (eq. sf-update)
 
@@ -115,9 +122,13 @@ def gate_select(layout: Layout, score: np.ndarray, s_tilde: np.ndarray, skip_run
 
     1. Frozen change (eq. delta-i): a region executed at the previous step takes
        its fresh score, a skipped one keeps its last value.
-    2. Per request b: D_b = sum_j (s~_j + eta)             (eq. gate-weight)
+    2. Per request b: D_b = sum_j (s~_j + eta)             (eq. gate-weight),
+       the binary64 terms fl(s~_j + eta) added one at a time in ascending
+       region order.
     3. Skip iff w_i = (s~_i + eta) / D_b < eps_b, evaluated without the division
-       as (s~_i + eta) < eps_b * D_b; eps_b = +inf skips every region.
+       as (s~_i + eta) < eps_b * D_b with the tie band TIE_BAND (an exact tie is
+       active; a NaN on either side compares false, so it is active too);
+       eps_b = +inf skips every region.
     4. Forced reactivation (eq. forced-reactivation): a region that has been
        skipped max_skip times in a row is active (max_skip = 0 disables it).
     Returns (s_tilde', skip_run', active) with active as bool [R].
@@ -135,7 +146,7 @@ def gate_select(layout: Layout, score: np.ndarray, s_tilde: np.ndarray, skip_run
         if np.isposinf(eps[b]):
             below = True
         else:
-            below = bool((s_t[r] + eta) < eps[b] * Db[b])
+            below = bool((s_t[r] + eta) < (eps[b] * Db[b]) * (1.0 - TIE_BAND))
         active[r] = forced or not below
     new_run = np.where(active, 0, skip_run.astype(np.int64) + 1).astype(np.int32)
     return s_t, new_run, active

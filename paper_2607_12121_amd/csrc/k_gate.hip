@@ -106,13 +106,14 @@ __global__ __launch_bounds__(kSelThreads) void gate_select_kernel(
   __syncthreads();
   for (int r = tid; r < R; r += kSelThreads) s_tilde[r] = st_s[r];
 
-  // 2. D_b = sum over the request's regions of (s~ + eta)
-  for (int b = wave; b < B; b += kSelWaves) {
+  // 2. D_b = sum over the request's regions of fl(s~ + eta), added one at a time in
+  //    ascending region order: a fixed order, so that D_b rounds the same way in
+  //    every evaluation of the gate and the decisions are reproducible bit for bit.
+  for (int b = tid; b < B; b += kSelThreads) {
     const int lo = req_reg_off[b], hi = req_reg_off[b + 1];
     double s = 0.0;
-    for (int r = lo + lane; r < hi; r += fd::kWave) s += st_s[r] + eta;
-    s = fd::wave_sum(s);
-    if (lane == 0) d_s[b] = s;
+    for (int r = lo; r < hi; ++r) s += st_s[r] + eta;
+    d_s[b] = s;
   }
   __syncthreads();
 
@@ -122,7 +123,10 @@ __global__ __launch_bounds__(kSelThreads) void gate_select_kernel(
     const double e = eps[b];
     const int run = skip_run[r];
     const bool forced = max_skip > 0 && run >= max_skip;
-    const bool below = (e == INFINITY) ? true : ((st_s[r] + eta) < e * d_s[b]);
+    // below the threshold: fl(s~ + eta) < fl(eps D_b) (1 - 2^-40).  The band makes every
+    // exact-arithmetic tie active (D_b's rounding error is below 2^-40 relative for
+    // R <= 4096); NaN compares false (active).
+    const bool below = (e == INFINITY) ? true : ((st_s[r] + eta) < (e * d_s[b]) * (1.0 - 0x1p-40));
     const bool act = forced || !below;
     act_s[r] = act ? 1 : 0;
     active[r] = act ? 1 : 0;

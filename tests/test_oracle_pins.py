@@ -87,7 +87,28 @@ def test_gate_golden(case):
                                     eps, case["eta"], case["max_skip"])
     np.testing.assert_array_equal(act.astype(int), case["active"])
     np.testing.assert_array_equal(run, case["new_skip_run"])
-    np.testing.assert_array_equal(s_t, case["new_s_tilde"])
+    np.testing.assert_array_equal(s_t, np.array(case["new_s_tilde"], float))   # NaN == NaN here
+
+
+def test_gate_golden_notes_binary64_claims():
+    """The binary64 facts the tie and NaN cases rely on, evaluated with Python
+    floats (IEEE binary64) in the stated order: without the 2^-40 band the
+    region-order sums would skip the exact ties."""
+    d = 0.0
+    for _ in range(16):
+        d += 0.0 + 0.1
+    assert d == 1.6000000000000003 and 0.0625 * d > 0.1
+    assert not (0.1 < (0.0625 * d) * (1.0 - orc.TIE_BAND))
+    d = 0.0
+    for _ in range(64):
+        d += 0.0 + 0.3
+    assert 0.015625 * d == 0.3000000000000004 and 0.015625 * d > 0.3
+    assert not (0.3 < (0.015625 * d) * (1.0 - orc.TIE_BAND))
+    # the band is wider than the sum's rounding error for any R <= 4096 ...
+    assert 4097 * 2.0 ** -53 < orc.TIE_BAND
+    # ... and far below a 2^-21 margin
+    assert (1 - 2.0 ** -20) < (0.5 * (2 - 2.0 ** -20)) * (1.0 - orc.TIE_BAND)
+    assert math.isnan(float("nan") + 1.0) and not (1.0 < float("nan"))
 
 
 def test_gate_weights_sum_to_one_per_request():
