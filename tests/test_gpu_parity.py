@@ -73,6 +73,99 @@ def test_select_random_layouts_stateful(seed):
         st = orc.GateState(s_t, run, act)
 
 
+def _golden_gate_cases():
+    import json
+    import os
+    with open(os.path.join(os.path.dirname(__file__), "golden", "gate_cases.json")) as f:
+        return json.load(f)["cases"]
+
+
+@pytest.mark.parametrize("case", _golden_gate_cases(), ids=lambda c: c["name"])
+def test_select_golden_cases(case):
+    """The hand-derived gate cases (eq. gate-weight, eq. delta-i, eq.
+    forced-reactivation; ties, eta, per-request D, eps = inf, D = 0, NaN,
+    equal scores with a non-dyadic eta) through fd_select: mask, skip counters,
+    frozen scores bit-exact against the stated values and the oracle; index list,
+    offsets and count against the oracle."""
+    rr = np.array(case["req_of_region"])
+    R, B = len(rr), int(rr.max()) + 1
+    tok_off = np.searchsorted(rr, np.arange(B + 1))   # one token per region, request-major
+    lay = orc.Layout(np.arange(R), tok_off, R)
+    gh.say(f"golden select {case['name']}: R={R} B={B}")
+    plan = _plan_from_layout(lay)
+    score = np.array(case["score"], float)
+    s_in = np.array(case["s_tilde"], float)
+    run_in = np.array(case["skip_run"], np.int32)
+    prev = np.array(case["prev_active"], np.uint8)
+    eps = np.array([float(e) for e in case["eps"]])
+    d_st = torch.from_numpy(s_in).cuda()
+    d_run = torch.from_numpy(run_in).cuda()
+    d_prev = torch.from_numpy(prev).cuda()
+    d_act = torch.full((R,), 7, dtype=torch.uint8, device="cuda")
+    idx = torch.full((R,), -7, dtype=torch.int32, device="cuda")
+    cu = torch.zeros(B + 1, dtype=torch.int32, device="cuda")
+    m = torch.zeros(1, dtype=torch.int32, device="cuda")
+    fdl.fd_select(plan, torch.from_numpy(score).cuda(), torch.from_numpy(eps).cuda(), case["eta"], case["max_skip"],
+                  d_st, d_run, d_prev, d_act, idx, cu, m)
+    torch.cuda.synchronize()
+    s_t, run, act = orc.gate_select(lay, score, s_in, run_in, prev.astype(bool), eps, case["eta"], case["max_skip"])
+    got_act = d_act.cpu().numpy()
+    np.testing.assert_array_equal(got_act, np.array(case["active"], np.uint8))
+    np.testing.assert_array_equal(got_act.astype(bool), act)
+    np.testing.assert_array_equal(d_run.cpu().numpy(), np.array(case["new_skip_run"]))
+    np.testing.assert_array_equal(d_run.cpu().numpy(), run)
+    np.testing.assert_array_equal(d_st.cpu().numpy(), np.array(case["new_s_tilde"], float))   # NaN == NaN
+    oidx, ocu = orc.active_rows(lay, act)
+    M = int(m.item())
+    assert M == len(oidx)
+    np.testing.assert_array_equal(idx[:M].cpu().numpy(), oidx)
+    np.testing.assert_array_equal(cu.cpu().numpy(), ocu)
+    assert (idx[M:].cpu().numpy() == -7).all()
+
+
+def test_select_many_requests_and_regions():
+    """The per-request sums at the kernel's limits: 1024 requests of 1-6 regions
+    and one request of 4096 regions with equal scores and eta = 0.1 at
+    eps = 1/4096 (exact ties: all active)."""
+    rng = np.random.default_rng(41)
+    lay = random_gate_layout(rng, B=1024, max_regions=4, max_tokens=2)
+    plan = _plan_from_layout(lay)
+    R, N, B = lay.n_regions, len(lay.token_region), lay.n_requests
+    score = rng.random(R) ** 2
+    eps = rng.uniform(0.05, 0.4, B)
+    out = {}
+    for k, v in (("st", torch.zeros(R, dtype=torch.float64)), ("run", torch.zeros(R, dtype=torch.int32)),
+                 ("act", torch.ones(R, dtype=torch.uint8)), ("idx", torch.zeros(N, dtype=torch.int32)),
+                 ("cu", torch.zeros(B + 1, dtype=torch.int32)), ("m", torch.zeros(1, dtype=torch.int32))):
+        out[k] = v.cuda()
+    gh.say(f"select limits: R={R} N={N} B={B}")
+    fdl.fd_select(plan, torch.from_numpy(score).cuda(), torch.from_numpy(eps).cuda(), 0.01, 0, out["st"],
+                  out["run"], out["act"], out["act"], out["idx"], out["cu"], out["m"])
+    torch.cuda.synchronize()
+    _, _, act = orc.gate_select(lay, score, np.zeros(R), np.zeros(R, np.int32), np.ones(R, bool), eps, 0.01, 0)
+    np.testing.assert_array_equal(out["act"].cpu().numpy().astype(bool), act)
+    oidx, ocu = orc.active_rows(lay, act)
+    np.testing.assert_array_equal(out["cu"].cpu().numpy(), ocu)
+    np.testing.assert_array_equal(out["idx"][:len(oidx)].cpu().numpy(), oidx)
+    # one request of 4096 equal-score regions
+    R = 4096
+    lay = orc.Layout(np.arange(R), np.array([0, R]), R)
+    plan = _plan_from_layout(lay)
+    st = torch.zeros(R, dtype=torch.float64, device="cuda")
+    run = torch.zeros(R, dtype=torch.int32, device="cuda")
+    act_d = torch.ones(R, dtype=torch.uint8, device="cuda")
+    idx = torch.zeros(R, dtype=torch.int32, device="cuda")
+    cu = torch.zeros(2, dtype=torch.int32, device="cuda")
+    m = torch.zeros(1, dtype=torch.int32, device="cuda")
+    eps = np.array([1.0 / R])
+    fdl.fd_select(plan, torch.zeros(R, dtype=torch.float64, device="cuda"), torch.from_numpy(eps).cuda(), 0.1, 0,
+                  st, run, act_d, act_d, idx, cu, m)
+    torch.cuda.synchronize()
+    _, _, act = orc.gate_select(lay, np.zeros(R), np.zeros(R), np.zeros(R, np.int32), np.ones(R, bool), eps, 0.1, 0)
+    assert act.all()
+    assert int(m.item()) == R and bool(act_d.cpu().numpy().all())
+
+
 @pytest.mark.parametrize("name", ["tiny", "image", "video", "audio", "packed"])
 def test_score_select_gather_full_size(name):
     w = wl.WORKLOADS[name]
