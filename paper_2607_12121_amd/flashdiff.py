@@ -124,6 +124,30 @@ def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
     return t.data_ptr()
 
 
+_DT = {"f32": (torch.float32,), "f64": (torch.float64,), "i32": (torch.int32,), "u8": (torch.uint8,),
+       "b16": (torch.bfloat16, torch.int16, torch.uint16), "bytes": None}
+
+
+def _need(name: str, t: Optional[torch.Tensor], kind: str, numel: int, exact: bool = False,
+          optional: bool = False) -> None:
+    """Host-side check of one tensor argument before its pointer reaches the library:
+    on a GPU, contiguous, of the element type the C entry point reads (`kind`;
+    "b16" = any 2-byte bf16 bit pattern, "bytes" = any type) and with at least
+    (or, with exact=True, exactly) `numel` elements."""
+    if t is None:
+        if optional:
+            return
+        raise FlashDiffError(f"{name} is required")
+    if not t.is_cuda:
+        raise FlashDiffError(f"{name} must be a device tensor")
+    allowed = _DT[kind]
+    if allowed is not None and t.dtype not in allowed:
+        raise FlashDiffError(f"{name} must be {kind}, got {t.dtype}")
+    n = t.numel() if kind != "bytes" else t.numel() * t.element_size()
+    if (n != numel) if exact else (n < numel):
+        raise FlashDiffError(f"{name} holds {n} elements, needs {'exactly ' if exact else ''}{numel}")
+
+
 def _stream(stream: Optional[torch.cuda.Stream] = None) -> int:
     s = stream if stream is not None else torch.cuda.current_stream()
     return s.cuda_stream
@@ -196,6 +220,11 @@ def fd_region_score_ws_size(plan: Plan, C: int) -> int:
 
 
 def fd_region_score(plan: Plan, C: int, x_cur, x_prev, score, ws, stream=None) -> None:
+    N, R = plan.n_tokens, plan.n_regions
+    _need("x_cur", x_cur, "f32", N * C)
+    _need("x_prev", x_prev, "f32", N * C)
+    _need("score", score, "f64", R)
+    _need("ws", ws, "bytes", fd_region_score_ws_size(plan, C))
     _check("fd_region_score", lib().fd_region_score(ctypes.byref(plan.c), C, _ptr(x_cur), _ptr(x_prev),
                                                     _ptr(score), _ptr(ws), ws.numel() * ws.element_size(),
                                                     _stream(stream)))
@@ -203,17 +232,33 @@ def fd_region_score(plan: Plan, C: int, x_cur, x_prev, score, ws, stream=None) -
 
 def fd_select(plan: Plan, score, eps, eta: float, max_skip: int, s_tilde, skip_run, prev_active, active,
               idx, cu_q, m, stream=None) -> None:
+    N, R, B = plan.n_tokens, plan.n_regions, plan.n_requests
+    for n_, t_, k_, c_ in (("score", score, "f64", R), ("eps", eps, "f64", B), ("s_tilde", s_tilde, "f64", R),
+                           ("skip_run", skip_run, "i32", R), ("prev_active", prev_active, "u8", R),
+                           ("active", active, "u8", R), ("idx", idx, "i32", N), ("cu_q", cu_q, "i32", B + 1),
+                           ("m", m, "i32", 1)):
+        _need(n_, t_, k_, c_)
     _check("fd_select", lib().fd_select(ctypes.byref(plan.c), _ptr(score), _ptr(eps), FdGate(eta, max_skip),
                                         _ptr(s_tilde), _ptr(skip_run), _ptr(prev_active), _ptr(active),
                                         _ptr(idx), _ptr(cu_q), _ptr(m), _stream(stream)))
 
 
 def fd_gather(plan: Plan, C: int, x_cur, idx, m, xa, stream=None) -> None:
+    N = plan.n_tokens
+    _need("x_cur", x_cur, "f32", N * C)
+    _need("idx", idx, "i32", N)
+    _need("m", m, "i32", 1)
+    _need("xa", xa, "b16", N * C)
     _check("fd_gather", lib().fd_gather(ctypes.byref(plan.c), C, _ptr(x_cur), _ptr(idx), _ptr(m), _ptr(xa),
                                         _stream(stream)))
 
 
 def fd_embed(plan: Plan, d: FdDims, xa, w_e, b_e, pos, idx, m, h, stream=None) -> None:
+    N = plan.n_tokens
+    for n_, t_, k_, c_ in (("xa", xa, "b16", N * d.C), ("w_e", w_e, "b16", d.D * d.C), ("b_e", b_e, "f32", d.D),
+                           ("pos", pos, "f32", N * d.D), ("idx", idx, "i32", N), ("m", m, "i32", 1),
+                           ("h", h, "f32", N * d.D)):
+        _need(n_, t_, k_, c_)
     _check("fd_embed", lib().fd_embed(ctypes.byref(plan.c), ctypes.byref(d), _ptr(xa), _ptr(w_e), _ptr(b_e),
                                       _ptr(pos), _ptr(idx), _ptr(m), _ptr(h), _stream(stream)))
 
@@ -223,6 +268,10 @@ def fd_block_ws_size(plan: Plan, d: FdDims) -> int:
 
 
 def fd_adaln(d: FdDims, n_blocks: int, n_out: int, n_requests: int, w_ada, b_ada, cond, mod, stream=None) -> None:
+    _need("w_ada", w_ada, "b16", n_blocks * n_out * d.D)
+    _need("b_ada", b_ada, "f32", n_blocks * n_out)
+    _need("cond", cond, "f32", n_requests * d.D)
+    _need("mod", mod, "f32", n_blocks * n_requests * n_out)
     _check("fd_adaln", lib().fd_adaln(ctypes.byref(d), n_blocks, n_out, n_requests, _ptr(w_ada), _ptr(b_ada),
                                       _ptr(cond), _ptr(mod), _stream(stream)))
 
@@ -240,18 +289,32 @@ def final_weights(params: Dict[str, torch.Tensor]) -> FdFinalWeights:
 
 def fd_block_forward(plan: Plan, d: FdDims, w: FdBlockWeights, cond, h, idx, cu_q, m, k_cache, v_cache, ws,
                      stream=None) -> None:
+    N, B = plan.n_tokens, plan.n_requests
+    _need("cond", cond, "f32", B * d.D, optional=bool(w.mod))
+    for n_, t_, k_, c_ in (("h", h, "f32", N * d.D), ("idx", idx, "i32", N), ("cu_q", cu_q, "i32", B + 1),
+                           ("m", m, "i32", 1), ("k_cache", k_cache, "b16", N * d.D),
+                           ("v_cache", v_cache, "b16", N * d.D), ("ws", ws, "bytes", fd_block_ws_size(plan, d))):
+        _need(n_, t_, k_, c_)
     _check("fd_block_forward", lib().fd_block_forward(
         ctypes.byref(plan.c), ctypes.byref(d), ctypes.byref(w), _ptr(cond), _ptr(h), _ptr(idx), _ptr(cu_q),
         _ptr(m), _ptr(k_cache), _ptr(v_cache), _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
 
 
 def fd_final(plan: Plan, d: FdDims, w: FdFinalWeights, cond, h, cu_q, m, v, ws, stream=None) -> None:
+    N, B = plan.n_tokens, plan.n_requests
+    for n_, t_, k_, c_ in (("cond", cond, "f32", B * d.D), ("h", h, "f32", N * d.D), ("cu_q", cu_q, "i32", B + 1),
+                           ("m", m, "i32", 1), ("v", v, "f32", N * d.C), ("ws", ws, "bytes", fd_block_ws_size(plan, d))):
+        _need(n_, t_, k_, c_)
     _check("fd_final", lib().fd_final(ctypes.byref(plan.c), ctypes.byref(d), ctypes.byref(w), _ptr(cond), _ptr(h),
                                       _ptr(cu_q), _ptr(m), _ptr(v), _ptr(ws), ws.numel() * ws.element_size(),
                                       _stream(stream)))
 
 
 def fd_scatter_update(plan: Plan, C: int, x, v, idx, m, dt, vcache, active, skip_mode: int, stream=None) -> None:
+    N, R, B = plan.n_tokens, plan.n_regions, plan.n_requests
+    for n_, t_, k_, c_ in (("x", x, "f32", N * C), ("v", v, "f32", N * C), ("idx", idx, "i32", 1), ("m", m, "i32", 1),
+                           ("dt", dt, "f32", B), ("vcache", vcache, "f32", N * C), ("active", active, "u8", R)):
+        _need(n_, t_, k_, c_)
     _check("fd_scatter_update", lib().fd_scatter_update(ctypes.byref(plan.c), C, _ptr(x), _ptr(v), _ptr(idx),
                                                         _ptr(m), _ptr(dt), _ptr(vcache), _ptr(active),
                                                         skip_mode, _stream(stream)))
@@ -263,6 +326,13 @@ def fd_importance_ws_size(plan: Plan, d: FdDims) -> int:
 
 def fd_region_importance(plan: Plan, d: FdDims, block_ws, k_cache, idx, m, active, r_bar, delta, importance, ws,
                          stream=None) -> None:
+    N, R = plan.n_tokens, plan.n_regions
+    for n_, t_, k_, c_ in (("block_ws", block_ws, "bytes", fd_block_ws_size(plan, d)),
+                           ("k_cache", k_cache, "b16", N * d.D), ("idx", idx, "i32", N), ("m", m, "i32", 1),
+                           ("active", active, "u8", R), ("r_bar", r_bar, "f64", R), ("delta", delta, "f64", R),
+                           ("ws", ws, "bytes", fd_importance_ws_size(plan, d))):
+        _need(n_, t_, k_, c_)
+    _need("importance", importance, "f64", R, optional=True)
     _check("fd_region_importance", lib().fd_region_importance(
         ctypes.byref(plan.c), ctypes.byref(d), _ptr(block_ws), block_ws.numel() * block_ws.element_size(),
         _ptr(k_cache), _ptr(idx), _ptr(m), _ptr(active), _ptr(r_bar), _ptr(delta), _ptr(importance), _ptr(ws),
@@ -283,6 +353,10 @@ def fd_partition(req_tok_off, req_reg_off, saliency, token_region, ws, stream=No
         raise FlashDiffError("req_tok_off and req_reg_off must both have B + 1 entries")
     if saliency.element_size() != 2 or token_region.dtype != torch.int32:
         raise FlashDiffError("saliency must hold 16-bit values and token_region int32")
+    n = int(to[-1])
+    _need("saliency", saliency, "bytes", 2 * n, exact=True)
+    _need("token_region", token_region, "i32", n, exact=True)
+    _need("ws", ws, "bytes", fd_partition_ws_size(n, len(to) - 1))
     _check("fd_partition", lib().fd_partition(len(to) - 1, to.ctypes.data, ro.ctypes.data, _ptr(saliency),
                                               _ptr(token_region), _ptr(ws), ws.numel() * ws.element_size(),
                                               _stream(stream)))
@@ -294,9 +368,15 @@ def partition(saliency: torch.Tensor, req_tok_off, req_reg_off, stream=None) -> 
     N, B = int(saliency.numel()), len(req_tok_off) - 1
     out = torch.empty(N, dtype=torch.int32, device=saliency.device)
     ws = torch.empty(max(fd_partition_ws_size(N, B), 256), dtype=torch.uint8, device=saliency.device)
+    if stream is not None:
+        # the buffers come from the current stream's pool and the saliency may still be
+        # written there: the launch stream waits for that work, and both buffers are
+        # marked as used on it (ws is freed here while the kernel may still run)
+        stream.wait_stream(torch.cuda.current_stream())
     fd_partition(req_tok_off, req_reg_off, saliency, out, ws, stream)
-    if stream is not None:   # the workspace is freed here while the kernel may still run on `stream`
+    if stream is not None:
         ws.record_stream(stream)
+        out.record_stream(stream)
     return out
 
 

@@ -13,6 +13,18 @@ from paper_2607_12121_amd import workloads as wl
 HEADER = os.path.join(os.path.dirname(os.path.dirname(__file__)), "include", "flashdiff.h")
 
 
+def _gpu_visible() -> bool:
+    import torch
+    return torch.cuda.device_count() > 0
+
+
+# These tests hand dummy addresses (0x1000) to entry points and rely on the
+# argument validation rejecting the call before any launch.  Where a GPU is
+# visible a regression in that validation would enqueue a kernel on them, so
+# they run only on hosts without one (the CPU tier).
+no_gpu = pytest.mark.skipif(_gpu_visible(), reason="passes dummy device addresses; CPU-only hosts")
+
+
 def _declared():
     src = open(HEADER).read()
     src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
@@ -63,6 +75,7 @@ def _fake_plan():
     return fdl.FdPlan(16, 4, 1, 4, 16, *([0x1000] * 6))
 
 
+@no_gpu
 def test_entry_points_validate_before_launch():
     lib = fdl.lib()
     plan = _fake_plan()
@@ -112,6 +125,7 @@ def test_block_workspace_size_formula():
     assert rows + 4 * cus * (128 * 128 * 4 + 4) <= got <= rows + 4 * cus * (256 * 256 * 4 + 4) + 8 * 256
 
 
+@no_gpu
 def test_adaln_validates_before_launch():
     lib = fdl.lib()
     d = fdl.FdDims(64, 128, 2, 64, 256)
@@ -129,6 +143,7 @@ def test_adaln_validates_before_launch():
     assert lib.fd_block_forward(ctypes.byref(plan), ctypes.byref(d), ctypes.byref(w0), *small) == 1   # no modulation
 
 
+@no_gpu
 def test_importance_validates_before_launch():
     lib = fdl.lib()
     plan = _fake_plan()
@@ -152,6 +167,7 @@ def test_importance_validates_before_launch():
     assert b"LDS" in lib.fd_last_error()
 
 
+@no_gpu
 def test_partition_validates_before_launch():
     lib = fdl.lib()
     to = np.array([0, 100, 300], np.int32)
@@ -192,3 +208,34 @@ def test_binding_fails_loudly_without_the_library(tmp_path):
     out = subprocess.run([sys.executable, "-c", code], env=env, cwd=root, capture_output=True, text=True,
                          timeout=300)
     assert out.returncode == 0 and "raised:" in out.stdout and "missing" in out.stdout, out.stderr[-2000:]
+
+
+def test_binding_rejects_host_tensors_and_bad_sizes():
+    """The wrappers check every tensor before its pointer reaches the library:
+    a host tensor, a wrong element type or too few elements raise on the host."""
+    import torch
+    x = torch.zeros(16, 64)
+    with pytest.raises(fdl.FlashDiffError, match="device tensor"):
+        fdl._need("x", x, "f32", 16 * 64)
+    # the size and type rules themselves, on a stand-in that reports a device
+    class T:
+        is_cuda = True
+        def __init__(self, n, dtype, es=4):
+            self.n, self.dtype, self.es = n, dtype, es
+        def numel(self):
+            return self.n
+        def element_size(self):
+            return self.es
+    fdl._need("ok", T(10, torch.float32), "f32", 10)
+    fdl._need("bigger", T(11, torch.float32), "f32", 10)
+    with pytest.raises(fdl.FlashDiffError, match="needs exactly"):
+        fdl._need("exact", T(11, torch.float32), "f32", 10, exact=True)
+    with pytest.raises(fdl.FlashDiffError, match="holds 9"):
+        fdl._need("short", T(9, torch.float32), "f32", 10)
+    with pytest.raises(fdl.FlashDiffError, match="must be f64"):
+        fdl._need("eps", T(4, torch.float32), "f64", 4)
+    fdl._need("bf16 bits", T(8, torch.int16, 2), "b16", 8)
+    fdl._need("ws", T(300, torch.uint8, 1), "bytes", 256)
+    fdl._need("absent", None, "f64", 4, optional=True)
+    with pytest.raises(fdl.FlashDiffError, match="required"):
+        fdl._need("absent", None, "f64", 4)

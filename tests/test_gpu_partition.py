@@ -100,3 +100,32 @@ def test_partition_region_count_limits():
     reg_off = np.concatenate([[0], np.cumsum(r)]).astype(np.int32)
     sal = np.concatenate([rng.integers(0, int(rng.choice([2, 50, 65536])), k) for k in n]).astype(np.uint16)
     _check("64 requests", sal, tok_off, reg_off)
+
+
+def test_partition_binding_rejects_mismatched_sizes():
+    """The binding checks the buffers against the offsets before the call: a
+    saliency map of 60 tokens with offsets [0, 61] (whose workspace size would
+    still pass the library's rounded check) raises on the host, no launch."""
+    sal = torch.zeros(60, dtype=torch.int16, device="cuda")
+    out = torch.zeros(61, dtype=torch.int32, device="cuda")
+    ws = torch.empty(max(fdl.fd_partition_ws_size(61, 1), 256), dtype=torch.uint8, device="cuda")
+    with pytest.raises(fdl.FlashDiffError, match="saliency"):
+        fdl.fd_partition([0, 61], [0, 4], sal, out, ws)
+    with pytest.raises(fdl.FlashDiffError, match="token_region"):
+        fdl.fd_partition([0, 60], [0, 4], sal, out, ws)
+
+
+def test_partition_on_a_side_stream_is_ordered_after_the_current_stream():
+    """partition(stream=s): the launch stream waits for the current stream's
+    writes to the saliency map (issued just before, not synchronised)."""
+    rq = wl.WORKLOADS["image"].requests[0]
+    sal = wl.saliency_map(rq, seed=5)
+    want = orc.otsu_partition(sal, rq.n_regions)
+    d_sal = torch.zeros(rq.n_tokens, dtype=torch.int16, device="cuda")
+    src = torch.from_numpy(sal.view(np.int16)).cuda()
+    torch.cuda.synchronize()
+    side = torch.cuda.Stream()
+    d_sal.copy_(src)                       # on the current stream
+    got = fdl.partition(d_sal, [0, rq.n_tokens], [0, rq.n_regions], stream=side)
+    side.synchronize()
+    np.testing.assert_array_equal(got.cpu().numpy(), want)
