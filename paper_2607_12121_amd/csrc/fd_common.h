@@ -49,11 +49,16 @@ FD_DEVICE int wave_sum(int v) {
   return v;
 }
 
-// Request of active row i: the b with cu_q[b] <= i < cu_q[b+1] (B is small; uniform loads).
+// Request of active row i < cu_q[B]: the b with cu_q[b] <= i < cu_q[b+1], found as the
+// largest b < B with cu_q[b] <= i (binary search over the ascending offsets; among
+// empty requests sharing an offset the largest one is the row's).  O(log B) loads.
 FD_DEVICE int row_request(const int32_t* __restrict__ cu_q, int B, int i) {
-  int b = 0;
-  while (b + 1 < B && cu_q[b + 1] <= i) ++b;
-  return b;
+  int lo = 0, hi = B - 1;   // cu_q[lo] <= i always (cu_q[0] = 0)
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (cu_q[mid] <= i) lo = mid; else hi = mid - 1;
+  }
+  return lo;
 }
 
 // GELU, tanh form: z/2 (1 + tanh(u)), u = sqrt(2/pi) (z + 0.044715 z^3).  Uses the

@@ -527,15 +527,19 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ACfg<D
         __hip_atomic_store(slot + (QG * DT * 16 + 2 * g + 1) * kThreads, l_run[g], __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
       }
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      // release this thread's partial at agent scope, count the arrival (acquire-release),
+      // and on the last piece acquire before reading the others: the pieces may have run
+      // on other XCDs
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
       __syncthreads();
       if (tid == 0) {
-        const int prev = __hip_atomic_fetch_add(&counters[share0], 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        const int prev = __hip_atomic_fetch_add(&counters[share0], 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
         s_last = (prev == npieces - 1);
         if (prev == npieces - 1) __hip_atomic_store(&counters[share0], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
       __syncthreads();
       if (!s_last) return;
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
       // combine the pieces in key order
       auto piece_base = [&](int j) { return partial + static_cast<size_t>(slot_of(j)) * (E * kThreads) + tid; };
 #pragma unroll
