@@ -158,9 +158,12 @@ fd_status fd_region_score(const fd_plan* plan, int32_t C, const float* x_cur, co
 /* ---------------------------------------------------------------- select
  * Patch Gate for every region, then the active-token index list:
  *  1. frozen change (eq. delta-i): s~[r] = prev_active[r] ? score[r] : s~[r]
- *  2. D_b = sum over request b of (s~ + eta)                  (eq. gate-weight)
- *  3. skip iff (s~[r] + eta) < eps[b] * D_b, or eps[b] = +inf; a tie is active;
- *     NaN scores are active
+ *  2. D_b = sum over request b of (s~ + eta)                  (eq. gate-weight),
+ *     the binary64 terms added one at a time in ascending region order
+ *  3. skip iff fl(s~[r] + eta) < fl(eps[b] * D_b) * (1 - 2^-40), or eps[b] = +inf:
+ *     the division-free form of w_r < eps; the band keeps every exact-arithmetic
+ *     tie (w_r = eps) active whatever way D_b rounds; a NaN score compares false,
+ *     so it is active (and a NaN in D_b leaves its whole request active)
  *  4. forced active if max_skip > 0 and skip_run[r] >= max_skip (eq. forced-reactivation)
  *  5. skip_run[r] = active ? 0 : skip_run[r] + 1
  *  6. idx = ascending ids of tokens whose region is active; cu_q[b] = number of
@@ -181,6 +184,10 @@ fd_status fd_select(const fd_plan* plan, const double* score, const double* eps,
                     int32_t* idx, int32_t* cu_q, int32_t* m, fd_stream_t stream);
 
 /* ---------------------------------------------------------------- gather
+ * The restriction of the latent to the active patches (App. "Setup and
+ * Notation": x^(i), the latent restricted to patch P_i; the update rule
+ * evaluates the network only for i in the active set A_n; Sec. 4 Backend:
+ * workers execute their assigned patches), as the network's bf16 input rows:
  * xa[i][c] = bf16(x_cur[idx[i]][c]) for i < *m (round to nearest even).
  *   x_cur device fp32 [N][C]; idx device int32 [N]; m device int32 [1];
  *   xa device bf16 [N][C] (rows >= *m untouched).
@@ -189,6 +196,10 @@ fd_status fd_gather(const fd_plan* plan, int32_t C, const float* x_cur, const in
                     const int32_t* m, uint16_t* xa, fd_stream_t stream);
 
 /* ---------------------------------------------------------------- embed
+ * Token embedding of the DiT backbone (Sec. 2.1: the served models are
+ * Diffusion Transformers over latent tokens; the paper gives no block, this is
+ * the standard DiT patch embedding with a learned position table), on the
+ * active rows only:
  * h[i] = xa[i] W_e^T + b_e + pos[idx[i]] for i < *m (fp32 accumulate).
  *   xa device bf16 [N][C]; w_e device bf16 [D][C]; b_e device fp32 [D];
  *   pos device fp32 [N][D] (position table of every token); h device fp32 [N][D].
@@ -198,7 +209,9 @@ fd_status fd_embed(const fd_plan* plan, const fd_dims* dims, const uint16_t* xa,
                    float* h, fd_stream_t stream);
 
 /* ---------------------------------------------------------------- adaLN
- * Modulation of n_blocks stacked blocks in one pass over their weights:
+ * The conditioning of the DiT blocks (Sec. 2.1 DiT backbone; standard adaLN
+ * DiT block, which the paper does not spell out): modulation of n_blocks
+ * stacked blocks in one pass over their weights:
  *   mod[l][b][j] = sum_k W[l][j][k] * SiLU(cond[b][k]) + bias[l][j],  j < n_out
  * (the adaLN conditioning of the DiT blocks; it depends on cond only, so the
  * modulation of every block of a step can be formed before the first block).
@@ -299,6 +312,8 @@ fd_status fd_partition(int32_t n_requests, const int32_t* req_tok_off, const int
                        fd_stream_t stream);
 
 /* ---------------------------------------------------------------- final
+ * The network output f_theta^(i)(x_n, t_n) of the active patches (App. "Setup
+ * and Notation", FlashDiff update rule), through the standard DiT final layer:
  * v[i] = (LN(h_i) * (1 + scale) + shift) W_out^T + b_out, (shift, scale) =
  * SiLU(cond_b) W_ada^T + b_ada, for i < *m.  v device fp32 [N][C].
  * ws: device scratch of fd_block_ws_size bytes (the same size suffices).
@@ -326,7 +341,9 @@ fd_status fd_scatter_update(const fd_plan* plan, int32_t C, float* x, const floa
  * `capacity` launches).  The events carry no system-scope memory fence, so
  * arming the timer does not stall the stream around the timed kernel.
  * fd_timer_read synchronises on the recorded events and writes each launch's
- * duration in milliseconds; it returns the count.
+ * duration in milliseconds; it returns the count.  The timer is the library's
+ * only process-wide state (one per process, guarded by a mutex, measurement
+ * only): while it is armed, the matching launches of every thread are timed.
  */
 enum {
   FD_K_SCORE = 1, FD_K_SELECT, FD_K_GATHER, FD_K_EMBED, FD_K_ADALN, FD_K_LN,
