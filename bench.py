@@ -1,12 +1,15 @@
 #!/usr/bin/env python3
 """Throughput of the region-sparse DiT denoising step on one MI355X.
 
-Workload: 1024x1024 image DiT (64x64 = 4096 latent tokens, 64 channels, hidden
-1536, 24 heads x 64, MLP 6144, 24 blocks, bf16 weights), 64 regions of 8x8
-tokens, 26 of them active per step (1664 active tokens).  Inputs (weights,
-K/V caches, latents, thresholds) are seeded synthetic data resident in HBM
-before timing.  One step = region score, gate select, gather, embed, 24 DiT
-blocks on the active rows, final layer, scatter-update, all through the C ABI.
+Workload (the largest single-GPU configuration): video DiT, 21 latent frames x
+30 x 52 patches = 32760 tokens, 64 channels, hidden 1536, 12 heads x 128, MLP
+6144, 30 blocks, bf16 weights; 140 regions of 3x6x13 tokens, 42 of them active
+per step in a band that moves with the frame and the step (9828 active tokens).
+Inputs (weights, K/V caches, latents, thresholds) are seeded synthetic data
+resident in HBM before timing.  One step = region score, gate select, gather,
+embed, 30 DiT blocks on the active rows, final layer, scatter-update, all
+through the C ABI.  The image workload (4096 tokens, 24 blocks, 1664 active
+rows) is timed the same way as a secondary figure.
 
 Prints one JSON line: active tokens/s, ms/step, the roofline of the dominant
 kernel (timed live with HIP events around its launches) and the CPU oracle's
@@ -27,7 +30,7 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0          # MI355X HBM3E
-WORKLOAD = "image"
+WORKLOAD = "video"
 
 
 def parse():
@@ -37,9 +40,10 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--pool", type=int, default=4, help="distinct latent pairs cycled through")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--workload", default=WORKLOAD, help="image (default), video, audio, packed or tiny")
+    ap.add_argument("--workload", default=WORKLOAD, help="video (default), image, audio, packed or tiny")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU oracle sample")
     ap.add_argument("--no-hbm", action="store_true", help="skip the streaming-kernel bandwidth figures")
+    ap.add_argument("--no-secondary", action="store_true", help="skip the secondary image-workload figure")
     ap.add_argument("--trajectory", type=int, default=0, metavar="T",
                     help="instead of the benchmark: T chained steps per threshold and skip mode, deviation "
                          "of the final latent from the dense trajectory (prints its own JSON line)")
@@ -223,9 +227,15 @@ def traffic_per_launch(kernel: str, workload: str):
     return read_traffic(os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.txt"), srcs)
 
 
-def cpu_baseline(w, params_gpu, M_expected: int, budget_s: float):
-    """The oracle on the host cores: gate + a sample of DiT blocks + final + update
-    of the same workload; the step time is extrapolated to all L blocks."""
+def cpu_baseline(w, params_gpu, M_expected: int, budget_s: float, max_rows: int = 1024):
+    """The oracle on the host cores, on a bounded sample of one step of the same
+    workload: the gate and embedding of all rows, then DiT blocks run on a
+    sample of at most `max_rows` of the active rows (their keys and values
+    written to the cache, their queries attending to every token of the
+    request, their MLP) for as many blocks as fit the budget, then the final
+    layer and update of all rows.  Every per-block cost of the oracle is linear
+    in the rows it runs, so the step time is extrapolated as the sampled block
+    time x (active rows / sampled rows) x L."""
     import torch
     from threadpoolctl import threadpool_info
 
@@ -246,7 +256,10 @@ def cpu_baseline(w, params_gpu, M_expected: int, budget_s: float):
     treq = lay.token_request()[idx]
     h = orc.embed(inp.x_cur[idx].astype(np.float64), idx, p64["w_e"], p64["b_e"], p64["pos"])
     t_gate = time.perf_counter() - t0
+    M = len(idx)
     rng = np.random.default_rng(0)
+    sel = np.sort(rng.choice(M, min(M, max_rows), replace=False))
+    hs = h[sel]
     blocks, t_blocks = 0, 0.0
     while blocks < w.L and (blocks < 1 or t_blocks < budget_s):
         blk = {k: params_gpu[k][blocks].to("cpu", torch.float64).numpy()
@@ -254,7 +267,7 @@ def cpu_baseline(w, params_gpu, M_expected: int, budget_s: float):
         kc = rng.standard_normal((w.N, w.D))
         vc = rng.standard_normal((w.N, w.D))
         t1 = time.perf_counter()
-        h = orc.block_forward(h, idx, treq, lay, blk, cond, kc, vc, w.H)
+        hs = orc.block_forward(hs, idx[sel], treq[sel], lay, blk, cond, kc, vc, w.H)
         t_blocks += time.perf_counter() - t1
         blocks += 1
     t2 = time.perf_counter()
@@ -262,12 +275,13 @@ def cpu_baseline(w, params_gpu, M_expected: int, budget_s: float):
     orc.latent_update(inp.x_cur, v, idx, lay, wl.dt_per_request(w), np.zeros((w.N, w.C), np.float32), act,
                       orc.FREEZE)
     t_tail = time.perf_counter() - t2
-    t_step = t_gate + t_tail + t_blocks / blocks * w.L
+    t_step = t_gate + t_tail + t_blocks / blocks * (M / len(sel)) * w.L
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
-    return {"value": len(idx) / t_step, "unit": "active tokens/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"gate + embed + {blocks} of {w.L} DiT blocks + final + update of one {w.name} step "
-                      f"(M={len(idx)}), step time extrapolated to {w.L} blocks; "
-                      f"{t_gate + t_blocks + t_tail:.1f} s of CPU work; host nproc={os.cpu_count()}",
+    return {"value": M / t_step, "unit": "active tokens/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"one {w.name} step (M={M} active rows): gate + embed of all rows, {blocks} of {w.L} DiT "
+                      f"blocks on {len(sel)} sampled active rows (scaled by {M / len(sel):.2f} rows and to {w.L} "
+                      f"blocks), final + update of all rows; {t_gate + t_blocks + t_tail:.1f} s of CPU work; "
+                      f"host nproc={os.cpu_count()}",
             "seconds_per_step": t_step}
 
 
@@ -327,88 +341,43 @@ def main():
             torch.neg(src, out=dst)
         torch.cuda.synchronize()
         del src, dst
-    w = wl.WORKLOADS[args.workload]
-    rm = wl.region_map(w)
-    print(f"[bench] workload {w.name}: N={w.N} R={w.R} D={w.D} L={w.L}; drawing inputs on the GPU",
-          file=sys.stderr, flush=True)
-    params = wl.make_params(w, device="cuda")
-    kc, vc = wl.make_kv_cache(w, device="cuda")
-    plan = fdl.make_plan(rm.token_region, rm.req_tok_off, rm.n_regions)
-    d = fdl.dims(w.C, w.D, w.H, w.dh, w.F)
-    stp = fdl.SparseStep(plan, d, params, w.L, k_cache=kc, v_cache=vc)
-    pairs, expected_m = [], []
-    for i in range(args.pool):
-        inp = wl.step_inputs(w, i, rmap=rm)
-        pairs.append((torch.from_numpy(inp.x_cur).cuda(), torch.from_numpy(inp.x_prev).cuda(),
-                      torch.from_numpy(inp.eps).cuda()))
-        expected_m.append(int(inp.hot[rm.token_region].sum()))
-    cond = wl.make_cond(w, device="cuda")
-    dt = torch.from_numpy(wl.dt_per_request(w)).cuda()
     if args.trajectory > 0:
+        w = wl.WORKLOADS[args.workload]
+        rm = wl.region_map(w)
+        params = wl.make_params(w, device="cuda")
+        kc, vc = wl.make_kv_cache(w, device="cuda")
+        plan = fdl.make_plan(rm.token_region, rm.req_tok_off, rm.n_regions)
+        d = fdl.dims(w.C, w.D, w.H, w.dh, w.F)
+        cond = wl.make_cond(w, device="cuda")
+        dt = torch.from_numpy(wl.dt_per_request(w)).cuda()
         print(json.dumps(trajectory_study(torch, fdl, wl, w, rm, params, kc, vc, plan, d, cond, dt,
                                           args.trajectory)), flush=True)
         return 0
 
-    def run(i):
-        x, xp, eps = pairs[i % args.pool]
-        stp.step(x, xp, eps, dt, cond, stateless=True)
-
-    for i in range(args.warmup):
-        run(i)
-    torch.cuda.synchronize()
-
-    # per-kernel time per step (untimed calibration pass, one kernel type at a time)
-    per_kernel = {}
-    for name in (k for k in fdl.KERNELS if k not in ("importance", "partition")):
-        fdl.fd_timer_arm(name, 4 * w.L + 8)
-        run(0)
-        torch.cuda.synchronize()
-        ms = fdl.fd_timer_read(4 * w.L + 8)
-        fdl.fd_timer_disarm()
-        per_kernel[name] = (float(ms.sum()), len(ms))
-    mfma_kernels = ("gemm_qkv", "gemm_o", "gemm_mlp1", "gemm_mlp2", "attn")
-    dominant = max(mfma_kernels, key=lambda k: per_kernel[k][0])
-
-    # timed region: K steps, the dominant kernel's launches bracketed by HIP events
-    cap = args.steps * 2 * w.L + 8
-    fdl.fd_timer_arm(dominant, cap)
-    torch.cuda.synchronize()
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
-    t_start.record()
-    for i in range(args.steps):
-        run(args.warmup + i)
-    t_end.record()
-    torch.cuda.synchronize()
-    ms_total = t_start.elapsed_time(t_end)
-    dom_ms = fdl.fd_timer_read(cap)
-    fdl.fd_timer_disarm()
-    M = int(stp.m.item())
-    last = (args.warmup + args.steps - 1) % args.pool
-    assert M == expected_m[last], f"active rows {M} != designed {expected_m[last]}"
-    m_mean = float(np.mean([expected_m[(args.warmup + i) % args.pool] for i in range(args.steps)]))
-    regions_mean = m_mean * w.R / w.N
-    ms_step = ms_total / args.steps
-    dom_avg_ms = float(np.mean(dom_ms))
-    achieved = kernel_flops(dominant, w, M) / (dom_avg_ms * 1e-3) / 1e12
-    traffic = traffic_per_launch(dominant, w.name)
+    res = time_workload(torch, fdl, wl, args.workload, args.steps, args.warmup, args.pool)
+    w, M = res["w"], res["M"]
     out = {
         "metric": "active tokens/sec per region-sparse DiT step; % bf16 MFMA peak",
-        "value": m_mean / (ms_step * 1e-3),
+        "value": res["value"],
         "unit": "active tokens/s",
-        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step,
+        "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": res["ms_per_step"],
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": w.description, "tokens": w.N, "active_tokens": m_mean, "regions": w.R,
-                   "active_regions": regions_mean, "blocks": w.L, "hidden": w.D, "heads": w.H, "head_dim": w.dh,
-                   "mlp": w.F, "latent_channels": w.C, "gate": "stateless, eps at the designed gap",
-                   "parallelism": "single GPU"},
-        "step_mfma_frac": step_flops(w, M) / (ms_step * 1e-3) / (PEAK_BF16_TFLOPS * 1e12),
-        "roofline": {"kernel": dominant, "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS, "traffic": traffic,
-                     "launches": len(dom_ms), "avg_ms": dom_avg_ms},
-        "kernels_ms_per_step": {k: round(v[0], 4) for k, v in per_kernel.items()},
+        "config": res["config"],
+        "step_mfma_frac": res["step_mfma_frac"],
+        "roofline": res["roofline"],
+        "kernels_ms_per_step": res["kernels_ms_per_step"],
     }
-    out["importance"] = importance_cost(fdl, stp, run, w, M, args.warmup + args.steps)
+    out["importance"] = importance_cost(fdl, res["stp"], res["run"], w, M, args.warmup + args.steps)
+    params = res["params"]
+    del res
+    torch.cuda.empty_cache()
+    if not args.no_secondary and args.workload != "image":
+        print("[bench] secondary figure: the image workload", file=sys.stderr, flush=True)
+        sec = time_workload(torch, fdl, wl, "image", args.steps, args.warmup, args.pool)
+        out["secondary"] = {k: sec[k] for k in ("value", "unit", "ms_per_step", "config", "step_mfma_frac",
+                                                "roofline", "kernels_ms_per_step")}
+        del sec
+        torch.cuda.empty_cache()
     out["partition"] = partition_cost(torch, fdl, wl)
     if not args.no_hbm:
         print("[bench] streaming-kernel bandwidth (score, gather, scatter)", file=sys.stderr, flush=True)
@@ -418,6 +387,87 @@ def main():
         out["cpu_baseline"] = cpu_baseline(w, params, M, args.cpu_seconds)
     print(json.dumps(out), flush=True)
     return 0
+
+
+def time_workload(torch, fdl, wl, name: str, steps: int, warmup: int, pool: int) -> dict:
+    """Times `steps` region-sparse steps of workload `name` (inputs resident in HBM,
+    stateless gate at the designed thresholds) and the dominant MFMA kernel's
+    launches inside them; returns the figures and the objects used."""
+    w = wl.WORKLOADS[name]
+    rm = wl.region_map(w)
+    print(f"[bench] workload {w.name}: N={w.N} R={w.R} D={w.D} L={w.L}; drawing inputs on the GPU",
+          file=sys.stderr, flush=True)
+    params = wl.make_params(w, device="cuda")
+    kc, vc = wl.make_kv_cache(w, device="cuda")
+    plan = fdl.make_plan(rm.token_region, rm.req_tok_off, rm.n_regions)
+    d = fdl.dims(w.C, w.D, w.H, w.dh, w.F)
+    stp = fdl.SparseStep(plan, d, params, w.L, k_cache=kc, v_cache=vc)
+    pairs, expected_m = [], []
+    for i in range(pool):
+        inp = wl.step_inputs(w, i, rmap=rm)
+        pairs.append((torch.from_numpy(inp.x_cur).cuda(), torch.from_numpy(inp.x_prev).cuda(),
+                      torch.from_numpy(inp.eps).cuda()))
+        expected_m.append(int(inp.hot[rm.token_region].sum()))
+    cond = wl.make_cond(w, device="cuda")
+    dt = torch.from_numpy(wl.dt_per_request(w)).cuda()
+
+    def run(i):
+        x, xp, eps = pairs[i % pool]
+        stp.step(x, xp, eps, dt, cond, stateless=True)
+
+    for i in range(warmup):
+        run(i)
+    torch.cuda.synchronize()
+
+    # per-kernel time per step (untimed calibration pass, one kernel type at a time)
+    per_kernel = {}
+    for kname in (k for k in fdl.KERNELS if k not in ("importance", "partition")):
+        fdl.fd_timer_arm(kname, 4 * w.L + 8)
+        run(0)
+        torch.cuda.synchronize()
+        ms = fdl.fd_timer_read(4 * w.L + 8)
+        fdl.fd_timer_disarm()
+        per_kernel[kname] = (float(ms.sum()), len(ms))
+    mfma_kernels = ("gemm_qkv", "gemm_o", "gemm_mlp1", "gemm_mlp2", "attn")
+    dominant = max(mfma_kernels, key=lambda k: per_kernel[k][0])
+
+    # timed region: K steps, the dominant kernel's launches bracketed by HIP events
+    cap = steps * 2 * w.L + 8
+    fdl.fd_timer_arm(dominant, cap)
+    torch.cuda.synchronize()
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    t_start.record()
+    for i in range(steps):
+        run(warmup + i)
+    t_end.record()
+    torch.cuda.synchronize()
+    ms_total = t_start.elapsed_time(t_end)
+    dom_ms = fdl.fd_timer_read(cap)
+    fdl.fd_timer_disarm()
+    M = int(stp.m.item())
+    last = (warmup + steps - 1) % pool
+    assert M == expected_m[last], f"active rows {M} != designed {expected_m[last]}"
+    m_mean = float(np.mean([expected_m[(warmup + i) % pool] for i in range(steps)]))
+    ms_step = ms_total / steps
+    dom_avg_ms = float(np.mean(dom_ms))
+    achieved = kernel_flops(dominant, w, M) / (dom_avg_ms * 1e-3) / 1e12
+    print(f"[bench] {w.name}: {ms_step:.3f} ms/step, {dominant} {dom_avg_ms * 1e3:.1f} us/launch",
+          file=sys.stderr, flush=True)
+    return {
+        "w": w, "M": M, "stp": stp, "run": run, "params": params,
+        "value": m_mean / (ms_step * 1e-3), "unit": "active tokens/s", "ms_per_step": ms_step,
+        "config": {"workload": w.description, "tokens": w.N, "active_tokens": m_mean, "regions": w.R,
+                   "active_regions": m_mean * w.R / w.N, "blocks": w.L, "hidden": w.D, "heads": w.H,
+                   "head_dim": w.dh, "mlp": w.F, "latent_channels": w.C,
+                   "gate": "stateless, eps at the designed gap", "parallelism": "single GPU"},
+        "step_mfma_frac": step_flops(w, M) / (ms_step * 1e-3) / (PEAK_BF16_TFLOPS * 1e12),
+        "roofline": {"kernel": dominant, "bound": "mfma", "achieved": achieved, "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
+                     "traffic": traffic_per_launch(dominant, w.name), "launches": len(dom_ms),
+                     "avg_ms": dom_avg_ms},
+        "kernels_ms_per_step": {k: round(v[0], 4) for k, v in per_kernel.items()},
+    }
 
 
 if __name__ == "__main__":

@@ -309,12 +309,33 @@ def make_cond(w: Workload, step: int = 0, device: str = "cpu") -> torch.Tensor:
 
 def make_kv_cache(w: Workload, seed: int = 99, device: str = "cpu", layers: Optional[int] = None
                   ) -> Tuple[torch.Tensor, torch.Tensor]:
-    """Synthetic per-block K/V caches ~ N(0, 1), bf16 [L, N, D] each.
+    """Synthetic per-block K/V caches ~ N(0, 1), bf16 [L, N, D] each (round to
+    nearest even).
 
     Stands in for a cache filled by earlier steps when a test or timing run
-    does not start from a dense warm-up step.
+    does not start from a dense warm-up step.  On the host the values come from
+    numpy's PCG64 generator, one independent stream per block and tensor
+    (children 2l and 2l + 1 of one seed sequence: block l's keys and values),
+    drawn by a few threads at once: the 6 GB cache of the video model takes
+    seconds, and the values do not depend on the thread count.  On a GPU
+    device they come from torch's device generator (other values, same
+    distribution: timing runs only).
     """
     L = w.L if layers is None else layers
+    if device == "cpu":
+        from concurrent.futures import ThreadPoolExecutor
+        streams = np.random.SeedSequence([int(w.seed), 31, int(seed)]).spawn(2 * L)
+        k = torch.empty((L, w.N, w.D), dtype=torch.bfloat16)
+        v = torch.empty((L, w.N, w.D), dtype=torch.bfloat16)
+        dst = [t for l in range(L) for t in (k[l], v[l])]
+
+        def draw(i: int) -> None:
+            a = np.random.default_rng(streams[i]).standard_normal((w.N, w.D), dtype=np.float32)
+            dst[i].copy_(torch.from_numpy(a))   # fp32 -> bf16, round to nearest even
+
+        with ThreadPoolExecutor(max_workers=8) as ex:
+            list(ex.map(draw, range(2 * L)))
+        return k, v
     g = torch.Generator(device=device)
     g.manual_seed(int(w.seed) * 31 + seed)
     k = torch.empty((L, w.N, w.D), dtype=torch.bfloat16, device=device)
