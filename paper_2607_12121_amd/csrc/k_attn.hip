@@ -88,21 +88,27 @@ FD_DEVICE float half_sum(float v) {
 template <int DH>
 struct ACfg {
   // 32-query groups per wave (two would share every K/V fragment read, half the LDS
-  // reads per MFMA, at the cost of the registers the pipeline needs)
+  // reads per MFMA, but the pipeline's registers then leave one wave per SIMD, whose
+  // softmax no other wave hides: measured slower)
   static constexpr int QG = 1;
   static constexpr int QB = kWaves * QG * 32;           // queries per unit
   static constexpr int KCH = DH / 8;                    // 16-byte chunks per key row
   static constexpr int TILE = KB * KCH;                 // chunks of one K or V tile
   static constexpr int STAGE = 2 * TILE;                // K tile then V tile
-  // dh <= 64: software pipeline (S of tile t + 1 next to the softmax of tile t), four
-  // stages; dh = 128: plain loop, two stages (two workgroups per CU fit the LDS)
-  static constexpr bool PIPE = DH <= 64;
-  static constexpr int STAGES = PIPE ? 4 : 2;
+  // Software pipeline: S of tile t + 1 next to the softmax of tile t.  Head dim <= 64:
+  // a ring of four K|V stages.  Head dim 128: K and V in two-slot rings of their own
+  // (K two tiles ahead, V one), 64 KB, so that two workgroups share a CU.
+  static constexpr bool PIPE = true;
+  static constexpr bool SPLIT = DH >= 128;
+  static constexpr int STAGES = SPLIT ? 2 : 4;           // ring memory: STAGES x (K tile + V tile)
   static constexpr int LOADS = STAGE / 64 / kWaves;     // 1 KB wave-loads per wave per stage
   static constexpr int KS = DH / 16;                    // k16 steps of S^T over d
   static constexpr int DT = (DH + 31) / 32;             // 32-row tiles of O^T
   static constexpr int OCC = 2;                         // workgroups per CU
+  static constexpr bool CUT = true;                     // pieces of cut items combined in-kernel
   static_assert(STAGE % (64 * kWaves) == 0, "stage must split into whole wave-loads");
+  // split rings: the first half of a wave's loads fetch K blocks, the second half V blocks
+  static_assert(!SPLIT || (LOADS % 2 == 0 && TILE / 64 == kWaves * LOADS / 2), "K/V halves of the wave-loads");
   // K: 16 consecutive rows at one chunk -> distinct 16-byte bank groups
   static constexpr __host__ __device__ int fk(int r) {
     return KCH >= 16 ? (r & 15) : KCH == 8 ? ((r >> 1) & 7) : ((r >> 3) & (KCH - 1));
@@ -221,29 +227,55 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ACfg<D
       const int c = (lane % KCH) ^ (is_v ? C::fv(r) : C::fk(r));
       dma_off[q] = static_cast<uint32_t>(k_beg + r) * static_cast<uint32_t>(2 * D) + col2 + static_cast<uint32_t>(c * 16);
     }
-    auto issue = [&](int kt, int st) {
-      const uint32_t buf = ring_base + static_cast<uint32_t>(st * C::STAGE * 16);
+    // wave-loads q in [Q0, Q1) of key tile kt (global index): K blocks to kbuf, V
+    // blocks to vbuf, 1 KB per block
+    auto issue_q = [&](int kt, uint32_t kbuf, uint32_t vbuf, auto q0_tag, auto q1_tag) {
+      constexpr int Q0 = decltype(q0_tag)::value, Q1 = decltype(q1_tag)::value;
       if (kt < n_full) {
         const uint32_t soff = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(kt * KB * 2 * D));
 #pragma unroll
-        for (int q = 0; q < LOADS; ++q) {
+        for (int q = Q0; q < Q1; ++q) {
           const int blk = wave_u + kWaves * q;              // wave-uniform
-          lds_dma16(buf + static_cast<uint32_t>(blk * 64 * 16), dma_off[q], blk >= TILE_BLKS ? rs_v : rs_k, soff);
+          const bool is_v = blk >= TILE_BLKS;
+          const uint32_t dst = is_v ? vbuf + static_cast<uint32_t>((blk - TILE_BLKS) * 64 * 16)
+                                    : kbuf + static_cast<uint32_t>(blk * 64 * 16);
+          lds_dma16(dst, dma_off[q], is_v ? rs_v : rs_k, soff);
         }
       } else {
         const int k0 = k_beg + kt * KB;
 #pragma unroll
-        for (int q = 0; q < LOADS; ++q) {
+        for (int q = Q0; q < Q1; ++q) {
           const int blk = wave_u + kWaves * q;              // wave-uniform
           const bool is_v = blk >= TILE_BLKS;
           const int r = (blk - (is_v ? TILE_BLKS : 0)) * RPL + lane / KCH;
           const int c = (lane % KCH) ^ (is_v ? C::fv(r) : C::fk(r));
           const int key = min(k0 + r, k_end - 1);
           const uint32_t off = static_cast<uint32_t>(key) * static_cast<uint32_t>(2 * D) + col2 + static_cast<uint32_t>(c * 16);
-          lds_dma16(buf + static_cast<uint32_t>(blk * 64 * 16), off, is_v ? rs_v : rs_k);
+          const uint32_t dst = is_v ? vbuf + static_cast<uint32_t>((blk - TILE_BLKS) * 64 * 16)
+                                    : kbuf + static_cast<uint32_t>(blk * 64 * 16);
+          lds_dma16(dst, off, is_v ? rs_v : rs_k);
         }
       }
     };
+    using IQ0 = std::integral_constant<int, 0>;
+    using IQH = std::integral_constant<int, LOADS / 2>;
+    using IQL = std::integral_constant<int, LOADS>;
+    // LDS byte address of local key tile t's K and V
+    auto k_addr = [&](int t) -> uint32_t {
+      return C::SPLIT ? ring_base + static_cast<uint32_t>((t & 1) * C::TILE * 16)
+                      : ring_base + static_cast<uint32_t>((t % STAGES) * C::STAGE * 16);
+    };
+    auto v_addr = [&](int t) -> uint32_t {
+      return C::SPLIT ? ring_base + static_cast<uint32_t>((2 + (t & 1)) * C::TILE * 16)
+                      : ring_base + static_cast<uint32_t>(((t % STAGES) * C::STAGE + C::TILE) * 16);
+    };
+    // combined ring: key tile kt into stage st; split rings: K or V of local tile t
+    auto issue = [&](int kt, int st) {
+      const uint32_t buf = ring_base + static_cast<uint32_t>(st * C::STAGE * 16);
+      issue_q(kt, buf, buf + static_cast<uint32_t>(C::TILE * 16), IQ0{}, IQL{});
+    };
+    auto issue_k = [&](int t) { issue_q(kt0 + min(t, nkt - 1), k_addr(t), 0u, IQ0{}, IQH{}); };
+    auto issue_v = [&](int t) { issue_q(kt0 + min(t, nkt - 1), 0u, v_addr(t), IQH{}, IQL{}); };
 
     f32x16_t oacc[QG][DT];
 #pragma unroll
@@ -264,7 +296,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ACfg<D
     // S^T (64 keys x 32 queries per group) of tile t = K Q^T; each K fragment feeds every group
     auto s_tile = [&](int t, SAcc& sacc, auto ks_lo_tag, auto ks_hi_tag) {
       constexpr int KS_LO = decltype(ks_lo_tag)::value, KS_HI = decltype(ks_hi_tag)::value;
-      const uint32_t kt_addr = ring_base + static_cast<uint32_t>((t % STAGES) * C::STAGE * 16);
+      const uint32_t kt_addr = k_addr(t);
       const f32x16_t zero = {};
 #pragma unroll
       for (int ks = KS_LO; ks < KS_HI; ++ks)
@@ -347,7 +379,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ACfg<D
 
     // O^T (d x 32 queries) += V^T P^T for tile t; k-step st covers keys 16 st .. 16 st + 15
     auto pv_tile = [&](int t, PAcc& pk) {
-      const uint32_t vt_addr = ring_base + static_cast<uint32_t>(((t % STAGES) * C::STAGE + C::TILE) * 16);
+      const uint32_t vt_addr = v_addr(t);
 #pragma unroll
       for (int st = 0; st < 4; ++st) {
 #pragma unroll
@@ -383,20 +415,31 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ACfg<D
     using IK = std::integral_constant<int, KS>;
     const bool ragged = (k_beg + kt1 * KB > k_end);   // only the piece's last tile can hold keys past the end
     auto body = [&](int t, SAcc& cur, SAcc& nxt) {
-      wait_vm_barrier<AHEAD_WAIT>();
-      issue(kt0 + min(t + STAGES - 1, nkt - 1), (t + STAGES - 1) % STAGES);
+      if constexpr (C::SPLIT) {
+        // K of tile t + 1 and V of tile t (issued one iteration ago) have landed, and
+        // every wave is done with K of tile t and V of tile t - 1, whose slots refill
+        wait_vm_barrier<0>();
+        issue_k(t + 2);
+        issue_v(t + 1);
+      } else {
+        wait_vm_barrier<AHEAD_WAIT>();
+        issue(kt0 + min(t + STAGES - 1, nkt - 1), (t + STAGES - 1) % STAGES);
+      }
       float m_new[QG];
       s_tile(t + 1, nxt, I0{}, I1{});
       softmax_max(t, cur, m_new, std::integral_constant<bool, false>{});
-      if constexpr (QG == 1) {
-        // Hand-interleaved block: the P math of tile t (16 element pairs) with one or
-        // two MFMA jobs after each pair: first the rest of S(t + 1), then PV(t) per
-        // 16-key step once its P quarter exists.  The order is pinned per chunk.
-        const uint32_t kt_addr = ring_base + static_cast<uint32_t>(((t + 1) % STAGES) * C::STAGE * 16);
-        const uint32_t vt_addr = ring_base + static_cast<uint32_t>(((t % STAGES) * C::STAGE + C::TILE) * 16);
+      {
+        // Hand-interleaved block: the P math of tile t (16 element pairs per query
+        // group, quarter-major: quarter st of every group before quarter st + 1) with
+        // MFMA jobs after each pair: first the rest of S(t + 1), then PV(t) per 16-key
+        // step once that quarter of P exists in every group.  A job is one LDS operand
+        // read feeding the MFMAs of all QG groups.  The order is pinned per pair.
+        const uint32_t kt_addr = k_addr(t + 1);
+        const uint32_t vt_addr = v_addr(t);
         constexpr int NS = (KS - 1) * 2, NP = DT * 4, NJ = NS + NP;
-        constexpr int PER = (NJ + 15) / 16;
-        // job j = its LDS operand read (fetch) and its MFMA (run); reads run two jobs ahead
+        constexpr int NPAIR = 16 * QG;
+        constexpr int PER = (NJ + NPAIR - 1) / NPAIR;
+        // job j = its LDS operand read (fetch) and its MFMAs (run); reads run two jobs ahead
         auto fetch = [&](int j) -> u32x4_t {
           if (j < NS) {
             const int ks = 1 + j / 2, kh = j % 2;
@@ -417,15 +460,22 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ACfg<D
           const bf16x8_t a = __builtin_bit_cast(bf16x8_t, op);
           if (j < NS) {
             const int ks = 1 + j / 2, kh = j % 2;
-            nxt[0][kh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[0][ks], nxt[0][kh], 0, 0, 0);
+#pragma unroll
+            for (int g = 0; g < QG; ++g)
+              nxt[g][kh] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, qf[g][ks], nxt[g][kh], 0, 0, 0);
           } else {
             const int st = (j - NS) / DT, dt = (j - NS) % DT;
-            oacc[0][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pk[0][st], oacc[0][dt], 0, 0, 0);
+#pragma unroll
+            for (int g = 0; g < QG; ++g)
+              oacc[g][dt] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, pk[g][st], oacc[g][dt], 0, 0, 0);
           }
         };
-        // earliest pair after which job j may run: S jobs at once, PV(st) after P quarter st
-        auto earliest = [&](int j) { return j < NS ? 0 : 4 * ((j - NS) / DT) + 3; };
-        float lsum = 0.f;
+        // earliest pair after which job j may run: S jobs at once, PV(st) after the last
+        // pair of quarter st
+        auto earliest = [&](int j) { return j < NS ? 0 : 4 * QG * ((j - NS) / DT + 1) - 1; };
+        float lsum[QG];
+#pragma unroll
+        for (int g = 0; g < QG; ++g) lsum[g] = 0.f;
         int cursor = 0;
         u32x4_t op0 = fetch(0), op1 = fetch(1);   // operands of jobs cursor and cursor + 1
         auto next_job = [&]() {
@@ -435,15 +485,16 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ACfg<D
           op1 = op2;
         };
 #pragma unroll
-        for (int pp = 0; pp < 16; ++pp) {
-          const int kh = pp / 8, half = (pp / 4) % 2, e = 2 * (pp % 4);
-          const float p0 = __builtin_amdgcn_exp2f(fmaf(cur[0][kh][half * 8 + e], scale_log2, -m_new[0]));
-          const float p1 = __builtin_amdgcn_exp2f(fmaf(cur[0][kh][half * 8 + e + 1], scale_log2, -m_new[0]));
+        for (int pp = 0; pp < NPAIR; ++pp) {
+          const int st = pp / (4 * QG), g = (pp / 4) % QG, e = 2 * (pp % 4);
+          const int kh = st / 2, half = st % 2;
+          const float p0 = __builtin_amdgcn_exp2f(fmaf(cur[g][kh][half * 8 + e], scale_log2, -m_new[g]));
+          const float p1 = __builtin_amdgcn_exp2f(fmaf(cur[g][kh][half * 8 + e + 1], scale_log2, -m_new[g]));
           const fd::f32x2_t f = {p0, p1};
           const bf16x2_t pb = __builtin_convertvector(f, bf16x2_t);
-          lsum = __builtin_amdgcn_fdot2_f32_bf16(pb, bf16x2_t{(__bf16)1.0f, (__bf16)1.0f}, lsum, false);
-          pk[0][kh * 2 + half][e] = pb[0];
-          pk[0][kh * 2 + half][e + 1] = pb[1];
+          lsum[g] = __builtin_amdgcn_fdot2_f32_bf16(pb, bf16x2_t{(__bf16)1.0f, (__bf16)1.0f}, lsum[g], false);
+          pk[g][st][e] = pb[0];
+          pk[g][st][e + 1] = pb[1];
 #pragma unroll
           for (int k = 0; k < PER; ++k)
             if (cursor < NJ && earliest(cursor) <= pp) next_job();
@@ -452,14 +503,12 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ACfg<D
 #pragma unroll
         for (int k = 0; k < NJ; ++k)
           if (cursor < NJ) next_job();
-        l_run[0] += lsum;
-      } else {
-        s_tile(t + 1, nxt, I1{}, IK{});
-        softmax_p(cur, pk, m_new);
-        pv_tile(t, pk);
+#pragma unroll
+        for (int g = 0; g < QG; ++g) l_run[g] += lsum[g];
       }
     };
     auto tail = [&](int t, SAcc& cur, bool masked) {
+      if constexpr (C::SPLIT) wait_vm_barrier<0>();   // V of tile t was issued by the last body
       float m_new[QG];
       if (masked)
         softmax_max(t, cur, m_new, std::integral_constant<bool, true>{});
@@ -469,9 +518,16 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ACfg<D
       pv_tile(t, pk);
     };
     if constexpr (C::PIPE) {
+      if constexpr (C::SPLIT) {
+        issue_k(0);
+        issue_v(0);
+        issue_k(1);
+        wait_vm_barrier<LOADS>();   // K of tile 0 has landed (V 0 and K 1 may be in flight)
+      } else {
 #pragma unroll
-      for (int p = 0; p < STAGES - 1; ++p) issue(kt0 + min(p, nkt - 1), p);
-      wait_vm_barrier<(STAGES - 2) * LOADS>();
+        for (int p = 0; p < STAGES - 1; ++p) issue(kt0 + min(p, nkt - 1), p);
+        wait_vm_barrier<(STAGES - 2) * LOADS>();
+      }
       s_tile(0, sa, I0{}, IK{});
       int t = 0;
       for (; t + 2 <= nkt - 1; t += 2) {
@@ -511,7 +567,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ACfg<D
 #pragma unroll
     for (int g = 0; g < QG; ++g) l_run[g] = half_sum(l_run[g]);
 
-    if (npieces > 1) {
+    if (C::CUT && npieces > 1) {
       // store this piece's unnormalised O, max and sum (lane-major), count the arrival
       constexpr int E = QG * (DT * 16 + 2);
       float* slot = partial + static_cast<size_t>(slot_of(piece)) * (E * kThreads) + tid;
@@ -527,19 +583,21 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ACfg<D
         __hip_atomic_store(slot + (QG * DT * 16 + 2 * g + 1) * kThreads, l_run[g], __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
       }
-      // release this thread's partial at agent scope, count the arrival (acquire-release),
-      // and on the last piece acquire before reading the others: the pieces may have run
-      // on other XCDs
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");
+      // once the workgroup's stores are done, thread 0 counts the arrival with a release
+      // read-modify-write at agent scope, and the last piece acquires before it reads
+      // the others (the pieces may have run on other XCDs)
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
       __syncthreads();
       if (tid == 0) {
-        const int prev = __hip_atomic_fetch_add(&counters[share0], 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+        const int prev = __hip_atomic_fetch_add(&counters[share0], 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+        if (prev == npieces - 1) {
+          __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+          __hip_atomic_store(&counters[share0], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
         s_last = (prev == npieces - 1);
-        if (prev == npieces - 1) __hip_atomic_store(&counters[share0], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
       __syncthreads();
       if (!s_last) return;
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
       // combine the pieces in key order
       auto piece_base = [&](int j) { return partial + static_cast<size_t>(slot_of(j)) * (E * kThreads) + tid; };
 #pragma unroll
@@ -677,8 +735,12 @@ size_t attn_scratch_bytes(int dh) {
 hipError_t launch_attention(const uint16_t* q, const uint16_t* kc, const uint16_t* vc, uint16_t* o, int D, int H,
                             int dh, const int32_t* cu_q, const int32_t* req_tok_off, int B, int n_max,
                             int max_req_tokens, float* partial, int32_t* counters, float* lse, hipStream_t s) {
-  const int slots = 2 * num_cus();
-  const int max_units = (partial && counters) ? gemm_max_tiles() : 0;
+  const int occ = dh >= 128 ? ACfg<128>::OCC : ACfg<64>::OCC;
+  const int slots = occ * num_cus();
+  // head dim 128: every workgroup runs whole (head, query tile) items (the long key
+  // range of each item keeps the rounds balanced), so no piece is handed to another
+  // workgroup; smaller heads cut items into pieces combined by the last one
+  const int max_units = (partial && counters && dh < 128) ? gemm_max_tiles() : 0;
   // persistent grid: the resident slots, fewer when even one key tile per share
   // would leave some idle (upper bound on the items: every request adds at most
   // one partial query tile)
