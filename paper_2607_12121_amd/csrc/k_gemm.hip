@@ -306,9 +306,10 @@ FD_DEVICE void gemm_tiles(const fdh::GemmArgs& g, int slots, int M, uint4* ring_
 
     if (S > 1) {
       // Store this split's tile (lane-major: element e of thread t at e * THREADS + t)
-      // with device-coherent stores, release them at agent scope (every thread), and
-      // count the arrival with an acquire-release read-modify-write: the last split
-      // to arrive then reads every partial after its store, on whichever XCD it ran.
+      // with device-coherent stores; once the workgroup's stores are done, thread 0
+      // counts the arrival with a release read-modify-write at agent scope, and the
+      // last split to arrive acquires before it reads the partials (the splits may
+      // have run on other XCDs).
       float* slot = g.partial + static_cast<size_t>(v) * (BM * BN) + tid;
 #pragma unroll
       for (int i = 0; i < FM; ++i)
@@ -318,16 +319,19 @@ FD_DEVICE void gemm_tiles(const fdh::GemmArgs& g, int slots, int M, uint4* ring_
           for (int r = 0; r < 16; ++r)
             __hip_atomic_store(slot + ((i * FN + j) * 16 + r) * THREADS, acc[i][j][r], __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
-      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "agent");   // this thread's partials, before the arrival
-      __syncthreads();
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this wave's partials have been performed
+      __syncthreads();   // ... and happen before thread 0's release below (workgroup barrier)
       if (tid == 0) {
-        const int prev = __hip_atomic_fetch_add(&g.counters[tile], 1, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT);
+        const int prev = __hip_atomic_fetch_add(&g.counters[tile], 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+        if (prev == S - 1) {
+          // the last arrival: acquire every split's released partials, reset the counter
+          __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+          __hip_atomic_store(&g.counters[tile], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
         s_last = (prev == S - 1);
-        if (prev == S - 1) __hip_atomic_store(&g.counters[tile], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
       }
-      __syncthreads();
+      __syncthreads();   // thread 0's acquire happens before every thread's loads below
       if (!s_last) continue;
-      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");   // every split's partials, after the arrivals
       // Sum the S partials (this split's included) in split order with
       // device-coherent loads: the result does not depend on which split arrived last.
       const float* base = g.partial + static_cast<size_t>(tile) * S * (BM * BN) + tid;
