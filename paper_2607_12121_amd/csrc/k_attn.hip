@@ -39,7 +39,7 @@ namespace {
 
 constexpr int kXcds = 8;
 constexpr int KB = 64;                    // keys per tile
-constexpr int kWaves = 4, kThreads = kWaves * 64;
+constexpr int kMaxThreads = 512;        // largest workgroup (the partial slots are per thread)
 constexpr int kMaxQG = 2;
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
@@ -91,7 +91,12 @@ struct ACfg {
   // reads per MFMA, but the pipeline's registers then leave one wave per SIMD, whose
   // softmax no other wave hides: measured slower)
   static constexpr int QG = 1;
-  static constexpr int QB = kWaves * QG * 32;           // queries per unit
+  // Waves per workgroup.  Head dim 128: eight (two per SIMD) in one workgroup per CU,
+  // so every K/V tile brought into LDS serves 256 queries (half the LDS writes per
+  // query of two four-wave workgroups); head dim <= 64: four, two workgroups per CU.
+  static constexpr int WAVES = DH >= 128 ? 8 : 4;
+  static constexpr int THREADS = WAVES * 64;
+  static constexpr int QB = WAVES * QG * 32;            // queries per unit
   static constexpr int KCH = DH / 8;                    // 16-byte chunks per key row
   static constexpr int TILE = KB * KCH;                 // chunks of one K or V tile
   static constexpr int STAGE = 2 * TILE;                // K tile then V tile
@@ -101,14 +106,16 @@ struct ACfg {
   static constexpr bool PIPE = true;
   static constexpr bool SPLIT = DH >= 128;
   static constexpr int STAGES = SPLIT ? 2 : 4;           // ring memory: STAGES x (K tile + V tile)
-  static constexpr int LOADS = STAGE / 64 / kWaves;     // 1 KB wave-loads per wave per stage
+  static constexpr int LOADS = STAGE / 64 / WAVES;      // 1 KB wave-loads per wave per stage
   static constexpr int KS = DH / 16;                    // k16 steps of S^T over d
   static constexpr int DT = (DH + 31) / 32;             // 32-row tiles of O^T
-  static constexpr int OCC = 2;                         // workgroups per CU
+  static constexpr int OCC = 8 / WAVES;                 // workgroups per CU
+  static constexpr int WPE = WAVES * OCC / 4;           // waves per SIMD
+  static_assert(THREADS <= kMaxThreads, "partial slots sized for kMaxThreads");
   static constexpr bool CUT = true;                     // pieces of cut items combined in-kernel
-  static_assert(STAGE % (64 * kWaves) == 0, "stage must split into whole wave-loads");
+  static_assert(STAGE % (64 * WAVES) == 0, "stage must split into whole wave-loads");
   // split rings: the first half of a wave's loads fetch K blocks, the second half V blocks
-  static_assert(!SPLIT || (LOADS % 2 == 0 && TILE / 64 == kWaves * LOADS / 2), "K/V halves of the wave-loads");
+  static_assert(!SPLIT || (LOADS % 2 == 0 && TILE / 64 == WAVES * LOADS / 2), "K/V halves of the wave-loads");
   // K: 16 consecutive rows at one chunk -> distinct 16-byte bank groups
   static constexpr __host__ __device__ int fk(int r) {
     return KCH >= 16 ? (r & 15) : KCH == 8 ? ((r >> 1) & 7) : ((r >> 3) & (KCH - 1));
@@ -134,7 +141,7 @@ FD_DEVICE bf16x8_t lds_read16(uint32_t addr) {
 }
 
 template <int DH>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ACfg<DH>::OCC, ACfg<DH>::OCC))) void attn_fwd_kernel(
+__global__ __launch_bounds__(ACfg<DH>::THREADS) __attribute__((amdgpu_waves_per_eu(ACfg<DH>::WPE, ACfg<DH>::WPE))) void attn_fwd_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ Kc, const uint16_t* __restrict__ Vc,
     uint16_t* __restrict__ O, int D, int H, const int32_t* __restrict__ cu_q, const int32_t* __restrict__ req_tok_off,
     int B, float scale_log2, float* __restrict__ partial, int32_t* __restrict__ counters, int max_units,
@@ -221,7 +228,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ACfg<D
     uint32_t dma_off[LOADS];
 #pragma unroll
     for (int q = 0; q < LOADS; ++q) {
-      const int blk = wave + kWaves * q;
+      const int blk = wave + C::WAVES * q;
       const bool is_v = blk >= TILE_BLKS;
       const int r = (blk - (is_v ? TILE_BLKS : 0)) * RPL + lane / KCH;   // key row within the tile
       const int c = (lane % KCH) ^ (is_v ? C::fv(r) : C::fk(r));
@@ -235,7 +242,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ACfg<D
         const uint32_t soff = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(kt * KB * 2 * D));
 #pragma unroll
         for (int q = Q0; q < Q1; ++q) {
-          const int blk = wave_u + kWaves * q;              // wave-uniform
+          const int blk = wave_u + C::WAVES * q;            // wave-uniform
           const bool is_v = blk >= TILE_BLKS;
           const uint32_t dst = is_v ? vbuf + static_cast<uint32_t>((blk - TILE_BLKS) * 64 * 16)
                                     : kbuf + static_cast<uint32_t>(blk * 64 * 16);
@@ -245,7 +252,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ACfg<D
         const int k0 = k_beg + kt * KB;
 #pragma unroll
         for (int q = Q0; q < Q1; ++q) {
-          const int blk = wave_u + kWaves * q;              // wave-uniform
+          const int blk = wave_u + C::WAVES * q;            // wave-uniform
           const bool is_v = blk >= TILE_BLKS;
           const int r = (blk - (is_v ? TILE_BLKS : 0)) * RPL + lane / KCH;
           const int c = (lane % KCH) ^ (is_v ? C::fv(r) : C::fk(r));
@@ -570,17 +577,17 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ACfg<D
     if (C::CUT && npieces > 1) {
       // store this piece's unnormalised O, max and sum (lane-major), count the arrival
       constexpr int E = QG * (DT * 16 + 2);
-      float* slot = partial + static_cast<size_t>(slot_of(piece)) * (E * kThreads) + tid;
+      float* slot = partial + static_cast<size_t>(slot_of(piece)) * (E * C::THREADS) + tid;
 #pragma unroll
       for (int g = 0; g < QG; ++g) {
 #pragma unroll
         for (int d = 0; d < DT; ++d)
 #pragma unroll
           for (int r = 0; r < 16; ++r)
-            __hip_atomic_store(slot + ((g * DT + d) * 16 + r) * kThreads, oacc[g][d][r], __ATOMIC_RELAXED,
+            __hip_atomic_store(slot + ((g * DT + d) * 16 + r) * C::THREADS, oacc[g][d][r], __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(slot + (QG * DT * 16 + 2 * g) * kThreads, m_run[g], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(slot + (QG * DT * 16 + 2 * g + 1) * kThreads, l_run[g], __ATOMIC_RELAXED,
+        __hip_atomic_store(slot + (QG * DT * 16 + 2 * g) * C::THREADS, m_run[g], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(slot + (QG * DT * 16 + 2 * g + 1) * C::THREADS, l_run[g], __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
       }
       // once the workgroup's stores are done, thread 0 counts the arrival with a release
@@ -599,10 +606,10 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ACfg<D
       __syncthreads();
       if (!s_last) return;
       // combine the pieces in key order
-      auto piece_base = [&](int j) { return partial + static_cast<size_t>(slot_of(j)) * (E * kThreads) + tid; };
+      auto piece_base = [&](int j) { return partial + static_cast<size_t>(slot_of(j)) * (E * C::THREADS) + tid; };
 #pragma unroll
       for (int g = 0; g < QG; ++g) {
-        const int mo = (QG * DT * 16 + 2 * g) * kThreads;
+        const int mo = (QG * DT * 16 + 2 * g) * C::THREADS;
         float m_all = -INFINITY;
         for (int s2 = 0; s2 < npieces; ++s2)
           m_all = fmaxf(m_all, __hip_atomic_load(piece_base(s2) + mo, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
@@ -618,9 +625,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(ACfg<D
           float pv[DT * 16];
 #pragma unroll
           for (int e = 0; e < DT * 16; ++e)
-            pv[e] = __hip_atomic_load(ps + (g * DT * 16 + e) * kThreads, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            pv[e] = __hip_atomic_load(ps + (g * DT * 16 + e) * C::THREADS, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
           const float ms = __hip_atomic_load(ps + mo, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          const float ls = __hip_atomic_load(ps + mo + kThreads, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          const float ls = __hip_atomic_load(ps + mo + C::THREADS, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
           __builtin_amdgcn_sched_barrier(0);
           const float w = (ms == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(ms - m_all);
           l_all += w * ls;
@@ -729,7 +736,7 @@ namespace fdh {
 size_t attn_scratch_bytes(int dh) {
   const size_t units = static_cast<size_t>(gemm_max_tiles());
   const size_t e = static_cast<size_t>(kMaxQG * (((dh + 31) / 32) * 16 + 2));
-  return units * e * kThreads * sizeof(float);
+  return units * e * kMaxThreads * sizeof(float);
 }
 
 hipError_t launch_attention(const uint16_t* q, const uint16_t* kc, const uint16_t* vc, uint16_t* o, int D, int H,
@@ -752,7 +759,7 @@ hipError_t launch_attention(const uint16_t* q, const uint16_t* kc, const uint16_
   grid = ((grid + kXcds - 1) / kXcds) * kXcds;
   const float scale_log2 = 1.4426950408889634f / sqrtf(static_cast<float>(dh));
 #define FD_ATTN_LAUNCH(DHV)                                                                                         \
-  attn_fwd_kernel<DHV><<<grid, kThreads, 0, s>>>(q, kc, vc, o, D, H, cu_q, req_tok_off, B, scale_log2, partial, counters, \
+  attn_fwd_kernel<DHV><<<grid, ACfg<DHV>::THREADS, 0, s>>>(q, kc, vc, o, D, H, cu_q, req_tok_off, B, scale_log2, partial, counters, \
                                                  max_units, lse)
   switch (dh) {
     case 16: FD_ATTN_LAUNCH(16); break;
