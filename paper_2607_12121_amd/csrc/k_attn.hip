@@ -105,7 +105,8 @@ struct ACfg {
   // (K two tiles ahead, V one), 64 KB, so that two workgroups share a CU.
   static constexpr bool PIPE = true;
   static constexpr bool SPLIT = DH >= 128;
-  static constexpr int STAGES = SPLIT ? 2 : 4;           // ring memory: STAGES x (K tile + V tile)
+  static constexpr int RING = 2;                         // slots of each split ring (3: modulo spills; 4: equal to 2)
+  static constexpr int STAGES = SPLIT ? RING : 4;        // ring memory: STAGES x (K tile + V tile)
   static constexpr int LOADS = STAGE / 64 / WAVES;      // 1 KB wave-loads per wave per stage
   static constexpr int KS = DH / 16;                    // k16 steps of S^T over d
   static constexpr int DT = (DH + 31) / 32;             // 32-row tiles of O^T
@@ -269,11 +270,11 @@ __global__ __launch_bounds__(ACfg<DH>::THREADS) __attribute__((amdgpu_waves_per_
     using IQL = std::integral_constant<int, LOADS>;
     // LDS byte address of local key tile t's K and V
     auto k_addr = [&](int t) -> uint32_t {
-      return C::SPLIT ? ring_base + static_cast<uint32_t>((t & 1) * C::TILE * 16)
+      return C::SPLIT ? ring_base + static_cast<uint32_t>((t % C::RING) * C::TILE * 16)
                       : ring_base + static_cast<uint32_t>((t % STAGES) * C::STAGE * 16);
     };
     auto v_addr = [&](int t) -> uint32_t {
-      return C::SPLIT ? ring_base + static_cast<uint32_t>((2 + (t & 1)) * C::TILE * 16)
+      return C::SPLIT ? ring_base + static_cast<uint32_t>((C::RING + t % C::RING) * C::TILE * 16)
                       : ring_base + static_cast<uint32_t>(((t % STAGES) * C::STAGE + C::TILE) * 16);
     };
     // combined ring: key tile kt into stage st; split rings: K or V of local tile t
@@ -423,11 +424,11 @@ __global__ __launch_bounds__(ACfg<DH>::THREADS) __attribute__((amdgpu_waves_per_
     const bool ragged = (k_beg + kt1 * KB > k_end);   // only the piece's last tile can hold keys past the end
     auto body = [&](int t, SAcc& cur, SAcc& nxt) {
       if constexpr (C::SPLIT) {
-        // K of tile t + 1 and V of tile t (issued one iteration ago) have landed, and
-        // every wave is done with K of tile t and V of tile t - 1, whose slots refill
-        wait_vm_barrier<0>();
-        issue_k(t + 2);
-        issue_v(t + 1);
+        // K of tile t + 1 and V of tile t (issued RING - 1 iterations ago) have landed,
+        // and every wave is done with K of tile t and V of tile t - 1, whose slots refill
+        wait_vm_barrier<(C::RING - 2) * LOADS>();
+        issue_k(t + C::RING);
+        issue_v(t + C::RING - 1);
       } else {
         wait_vm_barrier<AHEAD_WAIT>();
         issue(kt0 + min(t + STAGES - 1, nkt - 1), (t + STAGES - 1) % STAGES);
@@ -515,7 +516,7 @@ __global__ __launch_bounds__(ACfg<DH>::THREADS) __attribute__((amdgpu_waves_per_
       }
     };
     auto tail = [&](int t, SAcc& cur, bool masked) {
-      if constexpr (C::SPLIT) wait_vm_barrier<0>();   // V of tile t was issued by the last body
+      if constexpr (C::SPLIT) wait_vm_barrier<(C::RING - 2) * LOADS>();   // V of tile t has landed
       float m_new[QG];
       if (masked)
         softmax_max(t, cur, m_new, std::integral_constant<bool, true>{});
@@ -526,10 +527,13 @@ __global__ __launch_bounds__(ACfg<DH>::THREADS) __attribute__((amdgpu_waves_per_
     };
     if constexpr (C::PIPE) {
       if constexpr (C::SPLIT) {
-        issue_k(0);
-        issue_v(0);
-        issue_k(1);
-        wait_vm_barrier<LOADS>();   // K of tile 0 has landed (V 0 and K 1 may be in flight)
+#pragma unroll
+        for (int p = 0; p + 1 < C::RING; ++p) {
+          issue_k(p);
+          issue_v(p);
+        }
+        issue_k(C::RING - 1);
+        wait_vm_barrier<(C::RING - 1) * LOADS>();   // K of tile 0 has landed
       } else {
 #pragma unroll
         for (int p = 0; p < STAGES - 1; ++p) issue(kt0 + min(p, nkt - 1), p);
