@@ -155,6 +155,21 @@ size_t fd_region_score_ws_size(const fd_plan* plan, int32_t C);
 fd_status fd_region_score(const fd_plan* plan, int32_t C, const float* x_cur, const float* x_prev,
                           double* score, void* ws, size_t ws_bytes, fd_stream_t stream);
 
+/*
+ * The same region score for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): the partial sums live in a scratch array built into the library
+ * (1 MiB per GPU, held until the process ends), so no workspace is passed and
+ * nothing is allocated.  Arguments, layout and result as fd_region_score.
+ * FD_E_UNSUPPORTED (nothing enqueued) when fd_region_score_ws_size(plan, C)
+ * exceeds 1 MiB.  Every call on a GPU shares that GPU's scratch: calls that
+ * overlap on one GPU (concurrent streams or threads) race and must be ordered
+ * by the caller.  A call writes every partial it reads, so nothing left by an
+ * earlier call needs clearing.
+ */
+fd_status fd_region_score_noalloc(const fd_plan* plan, int32_t C, const float* x_cur, const float* x_prev,
+                                  double* score, fd_stream_t stream);
+
 /* ---------------------------------------------------------------- select
  * Patch Gate for every region, then the active-token index list:
  *  1. frozen change (eq. delta-i): s~[r] = prev_active[r] ? score[r] : s~[r]

@@ -245,6 +245,65 @@ fd_status fd_region_score(const fd_plan* plan, int32_t C, const float* x_cur, co
   return FD_OK;
 }
 
+// ---------------------------------------------------------------- region score without allocation
+// The partial sums of fd_region_score_noalloc live in this file-scope device array
+// (one copy per GPU, held until the process ends).  In host code its name is not a
+// device address: every host use goes through the address hipGetSymbolAddress
+// returns for the current device, taken once per device.
+}  // extern "C"
+
+namespace {
+
+constexpr size_t kScoreScratchBytes = size_t(1) << 20;   // 131072 (region, chunk) partial sums
+__device__ __align__(256) unsigned char scratch[kScoreScratchBytes];
+
+constexpr int kMaxDevices = 64;
+struct ScratchAddr {
+  std::once_flag once;
+  void* ptr = nullptr;
+  hipError_t err = hipSuccess;
+};
+ScratchAddr g_scratch[kMaxDevices];
+
+// Device address of `scratch` on the current device (looked up on the first call per device).
+fd_status scratch_address(void** out) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return fdh::hip_fail(e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fdh::set_error("device %d beyond the scratch table", dev), FD_E_UNSUPPORTED;
+  ScratchAddr& a = g_scratch[dev];
+  std::call_once(a.once, [&] { a.err = hipGetSymbolAddress(&a.ptr, HIP_SYMBOL(scratch)); });
+  if (a.err != hipSuccess || !a.ptr) return fdh::hip_fail(a.err, "hipGetSymbolAddress(scratch)");
+  *out = a.ptr;
+  return FD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+fd_status fd_region_score_noalloc(const fd_plan* plan, int32_t C, const float* x_cur, const float* x_prev,
+                                  double* score, fd_stream_t stream) {
+  FD_TRY(check_plan(plan));
+  FD_TRY(check_C(C));
+  FD_REQUIRE(x_cur && x_prev && score, "null pointer");
+  FD_REQUIRE(aligned(x_cur, 16) && aligned(x_prev, 16), "misaligned buffer");
+  const size_t need = fd_region_score_ws_size(plan, C);
+  if (need > kScoreScratchBytes)
+    return fdh::set_error("score partials need %zu bytes, beyond the %zu-byte built-in scratch (use fd_region_score)",
+                          need, kScoreScratchBytes),
+           FD_E_UNSUPPORTED;
+  void* ws = nullptr;
+  FD_TRY(scratch_address(&ws));
+  int rows = score_rows_per_chunk(C);
+  if (plan->n_regions >= 2 * fdh::num_cus()) rows = plan->max_region_tokens > 0 ? plan->max_region_tokens : 1;
+  const int nchunk = (plan->max_region_tokens + rows - 1) / rows;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  FD_LAUNCH(FD_K_SCORE, s,
+            fdh::launch_region_score(plan, C, x_cur, x_prev, score, static_cast<double*>(ws), nchunk, rows, s));
+  return FD_OK;
+}
+
 fd_status fd_select(const fd_plan* plan, const double* score, const double* eps, fd_gate gate, double* s_tilde,
                     int32_t* skip_run, const uint8_t* prev_active, uint8_t* active, int32_t* idx, int32_t* cu_q,
                     int32_t* m, fd_stream_t stream) {

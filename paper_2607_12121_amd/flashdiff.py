@@ -76,6 +76,7 @@ def lib() -> ctypes.CDLL:
         "fd_plan_build": ([_i32, _i32, _i32, _p, _p, _p, _p, _p, _p, _p, _p], _i32),
         "fd_region_score_ws_size": ([P(FdPlan), _i32], ctypes.c_size_t),
         "fd_region_score": ([P(FdPlan), _i32, _p, _p, _p, _p, ctypes.c_size_t, _p], _i32),
+        "fd_region_score_noalloc": ([P(FdPlan), _i32, _p, _p, _p, _p], _i32),
         "fd_select": ([P(FdPlan), _p, _p, FdGate, _p, _p, _p, _p, _p, _p, _p, _p], _i32),
         "fd_gather": ([P(FdPlan), _i32, _p, _p, _p, _p, _p], _i32),
         "fd_embed": ([P(FdPlan), P(FdDims), _p, _p, _p, _p, _p, _p, _p, _p], _i32),
@@ -105,6 +106,7 @@ def lib() -> ctypes.CDLL:
 
 def exported_symbols() -> Sequence[str]:
     return ("fd_last_error", "fd_version", "fd_plan_build", "fd_region_score_ws_size", "fd_region_score",
+            "fd_region_score_noalloc",
             "fd_select", "fd_gather", "fd_embed", "fd_adaln", "fd_block_ws_size", "fd_block_forward", "fd_final",
             "fd_scatter_update", "fd_importance_ws_size", "fd_region_importance", "fd_partition_ws_size",
             "fd_partition", "fd_timer_arm", "fd_timer_read", "fd_timer_disarm")
@@ -228,6 +230,16 @@ def fd_region_score(plan: Plan, C: int, x_cur, x_prev, score, ws, stream=None) -
     _check("fd_region_score", lib().fd_region_score(ctypes.byref(plan.c), C, _ptr(x_cur), _ptr(x_prev),
                                                     _ptr(score), _ptr(ws), ws.numel() * ws.element_size(),
                                                     _stream(stream)))
+
+
+def fd_region_score_noalloc(plan: Plan, C: int, x_cur, x_prev, score, stream=None) -> None:
+    """fd_region_score with the library's built-in scratch (no workspace argument)."""
+    N, R = plan.n_tokens, plan.n_regions
+    _need("x_cur", x_cur, "f32", N * C)
+    _need("x_prev", x_prev, "f32", N * C)
+    _need("score", score, "f64", R)
+    _check("fd_region_score_noalloc", lib().fd_region_score_noalloc(ctypes.byref(plan.c), C, _ptr(x_cur), _ptr(x_prev),
+                                                                    _ptr(score), _stream(stream)))
 
 
 def fd_select(plan: Plan, score, eps, eta: float, max_skip: int, s_tilde, skip_run, prev_active, active,
