@@ -91,10 +91,11 @@ struct ACfg {
   // reads per MFMA, but the pipeline's registers then leave one wave per SIMD, whose
   // softmax no other wave hides: measured slower)
   static constexpr int QG = 1;
-  // Waves per workgroup.  Head dim 128: eight (two per SIMD) in one workgroup per CU,
-  // so every K/V tile brought into LDS serves 256 queries (half the LDS writes per
-  // query of two four-wave workgroups); head dim <= 64: four, two workgroups per CU.
-  static constexpr int WAVES = DH >= 128 ? 8 : 4;
+  // Waves per workgroup.  Head dim 64 and 128: eight (two per SIMD) in one workgroup
+  // per CU, so every K/V tile brought into LDS serves 256 queries (half the LDS
+  // writes per query of two four-wave workgroups; video attention -8%, image -9%);
+  // head dim 16: four, two workgroups per CU.
+  static constexpr int WAVES = DH >= 64 ? 8 : 4;
   static constexpr int THREADS = WAVES * 64;
   static constexpr int QB = WAVES * QG * 32;            // queries per unit
   static constexpr int KCH = DH / 8;                    // 16-byte chunks per key row

@@ -125,15 +125,24 @@ FD_DEVICE void epilogue8(const fdh::GemmArgs& g, int row, int col, float v[8]) {
 
 // ---------------------------------------------------------------- tiled kernel
 
-template <int BM_, int BN_, int WM_, int WN_, int STAGES_, int OCC_>
+template <int BM_, int BN_, int WM_, int WN_, int STAGES_, int OCC_, int BK_ = 64, bool SPREAD_ = false>
 struct TileCfg {
-  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, STAGES = STAGES_, OCC = OCC_;
+  static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, STAGES = STAGES_, OCC = OCC_, BK = BK_;
+  // SPREAD: the next stage's loads are issued a share per k16 step, between the
+  // MFMAs, instead of all at once after the barrier
+  static constexpr bool SPREAD = SPREAD_;
   static constexpr int WAVES = WM * WN, THREADS = WAVES * 64;
   static constexpr int TM = BM / WM, TN = BN / WN, FM = TM / 32, FN = TN / 32;
-  static constexpr int CHUNKS = (BM + BN) * 8;              // 16-byte chunks per stage
-  static constexpr int LOADS = (BM + BN) / 8 / WAVES;       // 8-row wave-loads per wave per stage
-  static constexpr int LOADS_A = BM / 8 / WAVES;            // the first LOADS_A of them fetch A rows
-  static_assert(BM % (8 * WAVES) == 0 && BN % (8 * WAVES) == 0, "tile rows must split into 8-row wave-loads");
+  static constexpr int CPR = BK / 8;                        // 16-byte chunks per tile row
+  static constexpr int RPW = 64 / CPR;                      // tile rows per 1 KB wave-load
+  static constexpr int CHUNKS = (BM + BN) * CPR;            // 16-byte chunks per stage
+  static constexpr int LOADS = (BM + BN) / RPW / WAVES;     // wave-loads per wave per stage
+  static constexpr int LOADS_A = BM / RPW / WAVES;          // the first LOADS_A of them fetch A rows
+  static_assert(BK == 64 || BK == 32, "K step of 64 (eight chunks per row) or 32 (four)");
+  // chunk c of tile row r sits at c ^ swz(r): the 16 lanes reading one fragment (16
+  // consecutive rows, one logical chunk) hit 16 different 16-byte bank groups
+  static FD_DEVICE int swz(int r) { return BK == 64 ? (r >> 1) & 7 : (r >> 2) & 3; }
+  static_assert(BM % (RPW * WAVES) == 0 && BN % (RPW * WAVES) == 0, "tile rows must split into whole wave-loads");
   static_assert(TM % 32 == 0 && TN % 32 == 0, "wave tile must be whole 32x32 MFMA blocks");
   static_assert(STAGES * CHUNKS * 16 <= 160 * 1024, "ring exceeds LDS");
 };
@@ -183,7 +192,6 @@ FD_DEVICE void wait_vm_barrier() {
   asm volatile("s_waitcnt vmcnt(%0)\n\ts_barrier" : : "n"(N) : "memory");
 }
 
-FD_DEVICE int lds_swizzle(int row) { return (row >> 1) & 7; }
 
 // Number of K splits (identical in every WG): split only while every unit keeps
 // at least 24 K-steps and the units still fit the resident workgroup slots.
@@ -205,7 +213,8 @@ FD_DEVICE void gemm_tiles(const fdh::GemmArgs& g, int slots, int M, uint4* ring_
   const int tiles_m = (M + BM - 1) / BM;
   const int tiles_n = (N + BN - 1) / BN;
   const int tiles = tiles_m * tiles_n;
-  const int nk = K / TBK;
+  constexpr int BK = Cfg::BK, CPR = Cfg::CPR, RPW = Cfg::RPW;
+  const int nk = K / BK;
   const int S = (BM * BN == kSmallTile && g.max_units > 0) ? choose_split(tiles, nk, slots, g.max_units) : 1;
   const int units = tiles * S;
   const int per_xcd = (units + kXcds - 1) / kXcds;
@@ -232,19 +241,22 @@ FD_DEVICE void gemm_tiles(const fdh::GemmArgs& g, int slots, int M, uint4* ring_
 #pragma unroll
     for (int q = 0; q < LOADS; ++q) {
       const int blk = wave + WAVES * q;        // 8-row block in the concatenated A|B tile
-      const int r = blk * 8 + (lane >> 3);
-      const int c = (lane & 7) ^ lds_swizzle(r);
+      const int r = blk * RPW + lane / CPR;
+      const int c = (lane % CPR) ^ Cfg::swz(r);
       const int gr = (q < Cfg::LOADS_A) ? min(m0 + r, M - 1) : min(n0 + (r - BM), N - 1);
-      off[q] = static_cast<uint32_t>((static_cast<size_t>(gr) * K + c * 8) * 2);
+      off[q] = static_cast<uint32_t>((static_cast<size_t>(gr) * K + c * 8) * 2);   // chunk = 8 bf16
     }
-    auto issue = [&](int kt, int st) {
+    // wave-loads [q0, q1) of K-step kt into stage st
+    auto issue_q = [&](int kt, int st, int q0, int q1) {
       const uint32_t buf = ring_base + static_cast<uint32_t>(st * Cfg::CHUNKS * 16);
-      const uint32_t kb = static_cast<uint32_t>((kt0 + kt) * TBK * 2);
+      const uint32_t kb = static_cast<uint32_t>((kt0 + kt) * BK * 2);
 #pragma unroll
       for (int q = 0; q < LOADS; ++q)
-        lds_dma16(buf + static_cast<uint32_t>((wave_u + WAVES * q) * 64 * 16), off[q] + kb,
-                  q < Cfg::LOADS_A ? rs_a : rs_b);
+        if (q >= q0 && q < q1)
+          lds_dma16(buf + static_cast<uint32_t>((wave_u + WAVES * q) * 64 * 16), off[q] + kb,
+                    q < Cfg::LOADS_A ? rs_a : rs_b);
     };
+    auto issue = [&](int kt, int st) { issue_q(kt, st, 0, LOADS); };
 
     f32x16_t acc[FM][FN];
 #pragma unroll
@@ -260,7 +272,8 @@ FD_DEVICE void gemm_tiles(const fdh::GemmArgs& g, int slots, int M, uint4* ring_
       // exactly STAGES - 2 younger stages are in flight: stage `it` has landed for every wave
       wait_vm_barrier<(STAGES - 2) * LOADS>();
       // refill the slot every wave finished reading before this barrier (a repeat at the tail)
-      issue(min(it + STAGES - 1, nkt - 1), (it + STAGES - 1) % STAGES);
+      const int kt_next = min(it + STAGES - 1, nkt - 1), st_next = (it + STAGES - 1) % STAGES;
+      if constexpr (!Cfg::SPREAD) issue(kt_next, st_next);
       const uint4* sm = ring_mem + (it % STAGES) * Cfg::CHUNKS;
       bf16x8_t a[2][FM], b[2][FN];
       auto frag = [&](int ks, int slot) {
@@ -268,18 +281,22 @@ FD_DEVICE void gemm_tiles(const fdh::GemmArgs& g, int slots, int M, uint4* ring_
 #pragma unroll
         for (int i = 0; i < FM; ++i) {
           const int row = wm * TM + i * 32 + l32;
-          a[slot][i] = __builtin_bit_cast(bf16x8_t, sm[row * 8 + (ch ^ lds_swizzle(row))]);
+          a[slot][i] = __builtin_bit_cast(bf16x8_t, sm[row * CPR + (ch ^ Cfg::swz(row))]);
         }
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
           const int row = BM + wn * TN + j * 32 + l32;
-          b[slot][j] = __builtin_bit_cast(bf16x8_t, sm[row * 8 + (ch ^ lds_swizzle(row))]);
+          b[slot][j] = __builtin_bit_cast(bf16x8_t, sm[row * CPR + (ch ^ Cfg::swz(row))]);
         }
       };
       frag(0, 0);
 #pragma unroll
-      for (int ks = 0; ks < TBK / 16; ++ks) {
-        if (ks + 1 < TBK / 16) frag(ks + 1, (ks + 1) & 1);
+      for (int ks = 0; ks < BK / 16; ++ks) {
+        if (ks + 1 < BK / 16) frag(ks + 1, (ks + 1) & 1);
+        if constexpr (Cfg::SPREAD) {
+          constexpr int LQ = (LOADS + BK / 16 - 1) / (BK / 16);
+          issue_q(kt_next, st_next, ks * LQ, (ks + 1) * LQ);
+        }
 #pragma unroll
         for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -290,7 +307,7 @@ FD_DEVICE void gemm_tiles(const fdh::GemmArgs& g, int slots, int M, uint4* ring_
       // the first FM + FN MFMAs, then the remaining MFMAs
       __builtin_amdgcn_sched_group_barrier(0x100, FM + FN, 0);
 #pragma unroll
-      for (int ks = 0; ks < TBK / 16 - 1; ++ks) {
+      for (int ks = 0; ks < BK / 16 - 1; ++ks) {
 #pragma unroll
         for (int x = 0; x < FM + FN; ++x) {
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
