@@ -305,11 +305,12 @@ def test_gemm_tile_shapes_with_ragged_columns():
 
 
 def _attention_cuts_items(cu_q, req_tok_off, H, num_cus):
-    """Host mirror of the attention launch's schedule (query tiles of 128, key tiles
-    of 64, a grid of at most two workgroups per CU, 4 * num_cus partial slots): True
-    when the equal per-workgroup shares of the key-tile range may cut (head, query
-    tile) items, whose pieces are then combined by the last one to finish."""
-    QB, KB, slots, max_units = 128, 64, 2 * num_cus, 4 * num_cus
+    """Host mirror of the attention launch's schedule at head dim 64 (query tiles of
+    256 for the eight-wave workgroup, key tiles of 64, a grid of at most one
+    workgroup per CU, 4 * num_cus partial slots): True when the equal
+    per-workgroup shares of the key-tile range may cut (head, query tile) items,
+    whose pieces are then combined by the last one to finish."""
+    QB, KB, slots, max_units = 256, 64, num_cus, 4 * num_cus
     act = np.diff(cu_q)
     tok = np.diff(req_tok_off)
     nts = [-(-int(a) // QB) for a in act]
@@ -321,9 +322,10 @@ def _attention_cuts_items(cu_q, req_tok_off, H, num_cus):
 
 
 def test_attention_shares_cut_items_varlen():
-    """Three requests of 1024, 2048 and 512 tokens with 384 active rows each (144
-    (head, query tile) items over 8 to 32 key tiles): the attention's equal shares
-    cut items and cross request boundaries, so pieces of one item combine."""
+    """Three requests of 1024, 2048 and 512 tokens with 384 active rows each (96
+    (head, query tile) items over 8 to 32 key tiles, a ragged 128-row tile per
+    request): the attention's equal shares cut items and cross request
+    boundaries, so pieces of one item combine."""
     reqs = tuple(wl.RequestShape("seq", (n,), (32,)) for n in (1024, 2048, 512))
     w = small_workload("audio", requests=reqs, activity="count", activity_args=(12,), L=1)
     case = gh.make_case("audio", workload=w)
