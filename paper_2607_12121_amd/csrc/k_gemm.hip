@@ -125,8 +125,10 @@ FD_DEVICE void epilogue8(const fdh::GemmArgs& g, int row, int col, float v[8]) {
 
 // ---------------------------------------------------------------- tiled kernel
 
-template <int BM_, int BN_, int WM_, int WN_, int STAGES_, int OCC_, int BK_ = 64, bool SPREAD_ = false>
+template <int BM_, int BN_, int WM_, int WN_, int STAGES_, int OCC_, int BK_ = 64, bool SPREAD_ = false,
+          int GROUP_M_ = 0>
 struct TileCfg {
+  static constexpr int GROUP_M = GROUP_M_;   // tile order: groups of GROUP_M row tiles (0: row tile fastest)
   static constexpr int BM = BM_, BN = BN_, WM = WM_, WN = WN_, STAGES = STAGES_, OCC = OCC_, BK = BK_;
   // SPREAD: the next stage's loads are issued a share per k16 step, between the
   // MFMAs, instead of all at once after the barrier
@@ -151,7 +153,7 @@ using CfgWide = TileCfg<128, 192, 2, 2, 2, 2>;     // 1.5x the columns: one roun
 // half the columns: twice the tiles when few; its 24 KB stages fit three in the
 // shared ring, and the third stage hides the load latency that two exposed
 using CfgNarrow = TileCfg<128, 64, 2, 2, 3, 2>;
-using CfgLarge = TileCfg<256, 256, 2, 4, 2, 1>;
+using CfgLarge = TileCfg<256, 256, 2, 4, 2, 1, 64, false, 8>;   // tile order in groups of 8 row tiles
 constexpr int kSmallTile = 128 * 128;   // split-K partial tile (floats)
 // LDS ring of the two-workgroups-per-CU kernel: the largest of its three tile shapes
 constexpr int kSmallRing = CfgWide::STAGES * CfgWide::CHUNKS;
@@ -231,7 +233,20 @@ FD_DEVICE void gemm_tiles(const fdh::GemmArgs& g, int slots, int M, uint4* ring_
     const int v = (u % kXcds) * per_xcd + u / kXcds;
     if (v >= units) continue;
     const int tile = v / S, split = v - (v / S) * S;
-    const int tm = tile % tiles_m, tn = tile / tiles_m;
+    int tm, tn;
+    if constexpr (Cfg::GROUP_M > 0) {
+      // groups of GROUP_M row tiles x every column tile, row tile fastest: the tiles
+      // an XCD runs at once form a GROUP_M x (concurrent / GROUP_M) rectangle that
+      // shares its A and B panels in that XCD's L2
+      const int per_group = Cfg::GROUP_M * tiles_n;
+      const int grp = tile / per_group, r = tile - grp * per_group;
+      const int gm = min(Cfg::GROUP_M, tiles_m - grp * Cfg::GROUP_M);
+      tm = grp * Cfg::GROUP_M + r % gm;
+      tn = r / gm;
+    } else {
+      tm = tile % tiles_m;
+      tn = tile / tiles_m;
+    }
     const int m0 = tm * BM, n0 = tn * BN;
     const int kt0 = (split * nk) / S, kt1 = ((split + 1) * nk) / S;
     const int nkt = kt1 - kt0;
