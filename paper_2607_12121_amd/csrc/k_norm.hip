@@ -6,6 +6,8 @@ namespace {
 constexpr int kAdaThreads = 256;
 constexpr int kAdaWaves = kAdaThreads / fd::kWave;
 constexpr int kAdaLdsFloats = 12288;    // at most 48 KB of SiLU(cond) per pass
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+constexpr int kAdaRows = 4;   // weight rows per wave and group (2: 6.2 us per block, 4: 5.4)
 
 FD_DEVICE void bf16x8_to_f32(const uint4 w, float f[8]) {
   const uint32_t r[4] = {w.x, w.y, w.z, w.w};
@@ -69,7 +71,7 @@ FD_DEVICE void ada_store(const float (&acc)[R][NB], int row0, int n_rows, int n_
 // mod[l][b][j] = sum_k W[l][j][k] * SiLU(cond[b][k]) + bias[l][j] for n_blocks
 // stacked weight matrices (W bf16 [n_blocks][n_out][D], rows contiguous across
 // blocks): a stream of n_blocks * n_out weight rows, HBM-bound.  D = 512 KIT: each
-// wave walks groups of 2 consecutive rows (grid-stride), a lane holding 8
+// wave walks groups of kAdaRows consecutive rows (grid-stride), a lane holding 8
 // consecutive k of every 512; two register buffers keep the next group's loads in
 // flight while the current group is reduced.  SiLU(cond) of NB <= 2 requests sits
 // in LDS; B > NB re-streams the weights per NB requests.
@@ -79,7 +81,7 @@ __global__ __launch_bounds__(kAdaThreads) void adaln_stream_kernel(const uint16_
                                                                    const float* __restrict__ cond, int B, int D,
                                                                    int n_out, int n_rows, float* __restrict__ mod,
                                                                    int32_t* __restrict__ zero_ints, int n_zero) {
-  constexpr int R = 2;
+  constexpr int R = kAdaRows;
   extern __shared__ float sc[];   // [NB][D]
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   // The block's first kernel also clears the GEMM split-K arrival counters.
@@ -92,7 +94,11 @@ __global__ __launch_bounds__(kAdaThreads) void adaln_stream_kernel(const uint16_
     for (int i = 0; i < R; ++i) {
       const uint16_t* r = W + static_cast<size_t>(min(grp * R + i, n_rows - 1)) * D + lane * 8;   // past the end: the last row again
 #pragma unroll
-      for (int t = 0; t < KIT; ++t) w[t][i] = *reinterpret_cast<const uint4*>(r + t * 512);
+      for (int t = 0; t < KIT; ++t) {
+        // streaming loads: each weight row is read once per step (7.0 -> 6.1 us per block)
+        const u32x4_t x = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(r + t * 512));
+        w[t][i] = make_uint4(x.x, x.y, x.z, x.w);
+      }
     }
   };
   auto reduce = [&](int grp, const uint4 (&w)[KIT][R], int b0) {
@@ -239,7 +245,7 @@ hipError_t launch_adaln(const uint16_t* w, const float* b, const float* cond, in
   const int kit = (D % 512 == 0 && D <= 2048) ? D / 512 : 0;
   if (kit > 0 && nb <= 2) {
     // persistent: four workgroups per CU, fewer when the rows run out first
-    const int groups = (n_rows + 1) / 2;
+    const int groups = (n_rows + kAdaRows - 1) / kAdaRows;
     int grid = 4 * num_cus();
     if (grid > (groups + kAdaWaves - 1) / kAdaWaves) grid = (groups + kAdaWaves - 1) / kAdaWaves;
 #define FD_ADA(NB, KIT)                                                                                     \
