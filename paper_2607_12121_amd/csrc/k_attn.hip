@@ -335,15 +335,18 @@ __global__ __launch_bounds__(ACfg<DH>::THREADS) __attribute__((amdgpu_waves_per_
       }
 #pragma unroll
       for (int g = 0; g < QG; ++g) {
-        // two independent max3 chains over the 32 scores of this lane
-        float mx0 = __builtin_elementwise_maximum(sacc[g][0][0], sacc[g][0][1]);
-        float mx1 = __builtin_elementwise_maximum(sacc[g][1][0], sacc[g][1][1]);
+        // four independent max3 chains over the 32 scores of this lane
+        float mx[4];
 #pragma unroll
-        for (int r = 2; r < 16; r += 2) {
-          mx0 = max3(mx0, sacc[g][0][r], sacc[g][0][r + 1]);
-          mx1 = max3(mx1, sacc[g][1][r], sacc[g][1][r + 1]);
+        for (int c = 0; c < 4; ++c) {
+          const int kh = c >> 1, r0 = 8 * (c & 1);
+          mx[c] = __builtin_elementwise_maximum(sacc[g][kh][r0], sacc[g][kh][r0 + 1]);
+#pragma unroll
+          for (int r = r0 + 2; r < r0 + 8; r += 2) mx[c] = max3(mx[c], sacc[g][kh][r], sacc[g][kh][r + 1]);
         }
-        const float m_tile = half_max(__builtin_elementwise_maximum(mx0, mx1)) * scale_log2;
+        const float m_tile = half_max(__builtin_elementwise_maximum(__builtin_elementwise_maximum(mx[0], mx[1]),
+                                                                   __builtin_elementwise_maximum(mx[2], mx[3]))) *
+                             scale_log2;
         // Lazy rescaling: the subtracted max only moves when the tile max exceeds it by
         // more than 8 (P <= 2^8 otherwise); softmax does not depend on that constant.
         const bool grow = m_tile > m_run[g] + 8.0f;
@@ -482,9 +485,11 @@ __global__ __launch_bounds__(ACfg<DH>::THREADS) __attribute__((amdgpu_waves_per_
         // earliest pair after which job j may run: S jobs at once, PV(st) after the last
         // pair of quarter st
         auto earliest = [&](int j) { return j < NS ? 0 : 4 * QG * ((j - NS) / DT + 1) - 1; };
-        float lsum[QG];
+        float lsum[QG][4];   // four independent chains of row-sum dot products
 #pragma unroll
-        for (int g = 0; g < QG; ++g) lsum[g] = 0.f;
+        for (int g = 0; g < QG; ++g)
+#pragma unroll
+          for (int c = 0; c < 4; ++c) lsum[g][c] = 0.f;
         int cursor = 0;
         u32x4_t op0 = fetch(0), op1 = fetch(1);   // operands of jobs cursor and cursor + 1
         auto next_job = [&]() {
@@ -501,7 +506,7 @@ __global__ __launch_bounds__(ACfg<DH>::THREADS) __attribute__((amdgpu_waves_per_
           const float p1 = __builtin_amdgcn_exp2f(fmaf(cur[g][kh][half * 8 + e + 1], scale_log2, -m_new[g]));
           const fd::f32x2_t f = {p0, p1};
           const bf16x2_t pb = __builtin_convertvector(f, bf16x2_t);
-          lsum[g] = __builtin_amdgcn_fdot2_f32_bf16(pb, bf16x2_t{(__bf16)1.0f, (__bf16)1.0f}, lsum[g], false);
+          lsum[g][pp % 4] = __builtin_amdgcn_fdot2_f32_bf16(pb, bf16x2_t{(__bf16)1.0f, (__bf16)1.0f}, lsum[g][pp % 4], false);
           pk[g][st][e] = pb[0];
           pk[g][st][e + 1] = pb[1];
 #pragma unroll
@@ -513,7 +518,7 @@ __global__ __launch_bounds__(ACfg<DH>::THREADS) __attribute__((amdgpu_waves_per_
         for (int k = 0; k < NJ; ++k)
           if (cursor < NJ) next_job();
 #pragma unroll
-        for (int g = 0; g < QG; ++g) l_run[g] += lsum[g];
+        for (int g = 0; g < QG; ++g) l_run[g] += (lsum[g][0] + lsum[g][1]) + (lsum[g][2] + lsum[g][3]);
       }
     };
     auto tail = [&](int t, SAcc& cur, bool masked) {
