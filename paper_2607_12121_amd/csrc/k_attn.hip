@@ -3,19 +3,21 @@
 // ones).  Flash-style with an fp32 online softmax (base-2 exponent); both
 // contractions run on v_mfma_f32_32x32x16_bf16.
 //
-// Work item = (head, query tile of one request).  A workgroup of 4 waves
-// works on 128 queries at a time, 32 per wave (the code also supports two
-// 32-query groups per wave sharing every K/V fragment read; one group measured
-// faster once the loop is software-pipelined).  Each wave computes
+// Work item = (head, query tile of one request).  Head dim 64 and 128: one
+// workgroup of 8 waves per CU (two per SIMD) works on 256 queries at a time, 32
+// per wave; head dim 16: 4 waves, two workgroups per CU.  Each wave computes
 // S^T = K Q^T (keys x queries), so a lane owns one query column: its running max
 // needs one half-wave exchange per tile and its running sum none until the end;
-// S^T feeds O^T = V^T P^T directly as the B operand.  Head dim <= 64 runs a
-// software pipeline (S of the next key tile on the MFMA pipe beside the softmax of
-// the current one); head dim 128 a plain loop.  Two workgroups share a CU, so one
-// wave's softmax overlaps the other's MFMAs.
+// S^T feeds O^T = V^T P^T directly as the B operand.  Every head dim runs a
+// software pipeline: the iteration of key tile t issues the MFMAs of S(t + 1) and
+// of O += V P(t) as jobs between the element pairs of tile t's softmax, so one
+// wave's softmax runs beside MFMAs of its own and of the other wave on the SIMD.
+// (The code also supports two 32-query groups per wave sharing every K/V
+// fragment read; one group measured faster once the loop is pipelined.)
 //
 // K and V tiles of 64 keys stream from HBM straight into LDS (buffer_load ...
-// lds) through a ring of stages, both row-major in 16-byte chunks.  K rows are
+// lds), both row-major in 16-byte chunks: head dim 128 in two-slot rings of their
+// own (K two tiles ahead, V one), the others in one ring of K|V stages.  K rows are
 // read as MFMA A fragments (16 consecutive keys, one chunk): chunk c of key row
 // k sits at c ^ fk(k).  V^T is read with ds_read_b64_tr_b16: in a group of 16
 // lanes, lane j addresses 4 consecutive d of key K0 + j/4 and every lane
