@@ -44,6 +44,7 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU oracle sample")
     ap.add_argument("--no-hbm", action="store_true", help="skip the streaming-kernel bandwidth figures")
     ap.add_argument("--no-secondary", action="store_true", help="skip the secondary image-workload figure")
+    ap.add_argument("--no-trajectory", action="store_true", help="skip the chained-trajectory study")
     ap.add_argument("--trajectory", type=int, default=0, metavar="T",
                     help="instead of the benchmark: T chained steps per threshold and skip mode, deviation "
                          "of the final latent from the dense trajectory (prints its own JSON line)")
@@ -285,7 +286,8 @@ def cpu_baseline(w, params_gpu, M_expected: int, budget_s: float, max_rows: int 
             "seconds_per_step": t_step}
 
 
-def trajectory_study(torch, fdl, wl, w, rm, params, kc, vc, plan, d, cond, dt, T: int) -> dict:
+def trajectory_study(torch, fdl, wl, w, rm, params, kc, vc, plan, d, cond, dt, T: int,
+                     cs=(0.9, 0.95, 1.0, 1.05, 1.1, 1.2)) -> dict:
     """Chained steps x_{n+1} = x_n + dt v(x_n) from the same start, one dense warm-up
     step (eps = 0) then T - 1 gated steps (stateful gate, forced reactivation after
     K = 5 skips), for thresholds eps_b = c / R_b and both skip modes; reports the
@@ -313,11 +315,24 @@ def trajectory_study(torch, fdl, wl, w, rm, params, kc, vc, plan, d, cond, dt, T
     x_ref, _ = run(0.0, fdl.FD_SKIP_FREEZE)
     runs = []
     for mode, name in ((fdl.FD_SKIP_FREEZE, "freeze"), (fdl.FD_SKIP_REUSE_DRIFT, "reuse_drift")):
-        for c in (0.9, 0.95, 1.0, 1.05, 1.1, 1.2):
+        for c in cs:
             x, af = run(c, mode)
             dev = float(torch.linalg.vector_norm(x - x_ref) / torch.linalg.vector_norm(x_ref))
             runs.append({"mode": name, "eps_times_regions": c, "active_frac": af, "rel_dev": dev})
     return {"trajectory": {"workload": w.name, "steps": T, "max_skip": 5, "dt": float(dt[0].item()), "runs": runs}}
+
+
+def trajectory_for(torch, fdl, wl, name: str, T: int, **kw) -> dict:
+    """trajectory_study on workload `name` with its synthetic weights and caches."""
+    w = wl.WORKLOADS[name]
+    rm = wl.region_map(w)
+    params = wl.make_params(w, device="cuda")
+    kc, vc = wl.make_kv_cache(w, device="cuda")
+    plan = fdl.make_plan(rm.token_region, rm.req_tok_off, rm.n_regions)
+    d = fdl.dims(w.C, w.D, w.H, w.dh, w.F)
+    cond = wl.make_cond(w, device="cuda")
+    dt = torch.from_numpy(wl.dt_per_request(w)).cuda()
+    return trajectory_study(torch, fdl, wl, w, rm, params, kc, vc, plan, d, cond, dt, T, **kw)
 
 
 def main():
@@ -342,16 +357,7 @@ def main():
         torch.cuda.synchronize()
         del src, dst
     if args.trajectory > 0:
-        w = wl.WORKLOADS[args.workload]
-        rm = wl.region_map(w)
-        params = wl.make_params(w, device="cuda")
-        kc, vc = wl.make_kv_cache(w, device="cuda")
-        plan = fdl.make_plan(rm.token_region, rm.req_tok_off, rm.n_regions)
-        d = fdl.dims(w.C, w.D, w.H, w.dh, w.F)
-        cond = wl.make_cond(w, device="cuda")
-        dt = torch.from_numpy(wl.dt_per_request(w)).cuda()
-        print(json.dumps(trajectory_study(torch, fdl, wl, w, rm, params, kc, vc, plan, d, cond, dt,
-                                          args.trajectory)), flush=True)
+        print(json.dumps(trajectory_for(torch, fdl, wl, args.workload, args.trajectory)), flush=True)
         return 0
 
     res = time_workload(torch, fdl, wl, args.workload, args.steps, args.warmup, args.pool)
@@ -377,6 +383,12 @@ def main():
         out["secondary"] = {k: sec[k] for k in ("value", "unit", "ms_per_step", "config", "step_mfma_frac",
                                                 "roofline", "kernels_ms_per_step")}
         del sec
+        torch.cuda.empty_cache()
+    if not (args.no_trajectory or args.no_secondary) and args.workload != "image":
+        # the chained-trajectory study at two thresholds around the designed gap (with
+        # the secondary figures: runs that skip those, e.g. the profiled ones, skip it)
+        print("[bench] trajectory study: image, 50 chained steps", file=sys.stderr, flush=True)
+        out["trajectory"] = trajectory_for(torch, fdl, wl, "image", 50, cs=(1.0, 1.05))["trajectory"]
         torch.cuda.empty_cache()
     out["partition"] = partition_cost(torch, fdl, wl)
     if not args.no_hbm:
