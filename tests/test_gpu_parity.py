@@ -339,6 +339,26 @@ def test_attention_shares_cut_items_varlen():
     gh.compare_step(case, g, o, inp.x_cur, st)
 
 
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("base", ["audio", "video"])
+def test_many_requests_varlen(base):
+    """64 requests of 64 to 512 tokens (32-token regions, 20-70% of each request
+    active) through one block, head dim 64 (audio dims) and 128 (video dims):
+    the attention's schedule walks 64 requests' query tiles and key ranges, and
+    every row looks its request up among 64."""
+    rng = np.random.default_rng(64)
+    reqs = tuple(wl.RequestShape("seq", (32 * int(n),), (32,)) for n in rng.integers(2, 17, size=64))
+    w = small_workload(base, requests=reqs, activity="frac", activity_args=(0.2, 0.7), L=1)
+    case = gh.make_case(base, workload=w)
+    inp = case.inp
+    gh.say(f"many requests ({base} dims): B={w.B} N={w.N} R={w.R}")
+    g, st = gh.run_gpu(case, inp.eps, inp.x_cur, inp.x_prev)
+    assert len(g["cu_q"]) == 65 and g["M"] > 0
+    o = gh.run_oracle(case, inp.eps, inp.x_cur, inp.x_prev)
+    errs = gh.compare_step(case, g, o, inp.x_cur, st)
+    gh.say(f"  M={g['M']}: " + ", ".join(f"{k}={v:.2e}" for k, v in errs.items()))
+
+
 def test_single_region_and_single_token_regions():
     reqs = (wl.RequestShape("grid2d", (8, 8), (8, 8)), wl.RequestShape("grid2d", (4, 12), (1, 1)))
     w = small_workload("tiny", requests=reqs, activity="frac", activity_args=(0.3, 0.6), L=1)
