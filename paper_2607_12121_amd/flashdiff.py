@@ -491,3 +491,16 @@ class SparseStep:
                                      self.delta, self.importance, self.ws_imp, stream)
         fd_final(p, d, self.final_w, cond, self.h, self.cu_q, self.m, self.v, self.ws_block, stream)
         fd_scatter_update(p, C, x, self.v, self.idx, self.m, dt, self.vcache, self.active, skip_mode, stream)
+
+    def capture(self, x: torch.Tensor, x_prev: torch.Tensor, eps: torch.Tensor, dt: torch.Tensor,
+                cond: torch.Tensor, **kw) -> "torch.cuda.CUDAGraph":
+        """Records one step on these tensors into a HIP graph (nothing runs during the
+        capture); each replay() runs the step on whatever the tensors then hold, with
+        the same state buffers as step().  The step makes no host round trip and no
+        allocation, and every counter its kernels rely on is cleared by a kernel of the
+        step itself, so replays are independent of each other.  Keyword arguments are
+        those of step() except `stream`."""
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            self.step(x, x_prev, eps, dt, cond, **kw)
+        return g
