@@ -28,7 +28,7 @@ struct BlockWs {
   uint16_t* o;
   uint16_t* g;
   float* partial;      // split-K partial tiles
-  int32_t* counters;   // split-K arrival counters (zeroed at the start of every block)
+  int32_t* counters;   // arrival counters of cut attention items (zeroed at the start of every block)
   float* lse;          // [N][H] base-2 log-sum-exp of each active query's scaled scores
   size_t bytes;
 };
@@ -49,7 +49,7 @@ BlockWs carve_block_ws(const fd_plan* p, const fd_dims* d, void* base) {
   w.o = static_cast<uint16_t*>(take(n * d->D * 2));
   w.g = static_cast<uint16_t*>(take(n * d->F * 2));
   const size_t tiles = static_cast<size_t>(fdh::gemm_max_tiles());
-  const size_t gemm_part = fdh::gemm_scratch_bytes() - tiles * sizeof(int32_t);
+  const size_t gemm_part = fdh::gemm_scratch_bytes();
   const size_t attn_part = fdh::attn_scratch_bytes(d->dh);
   w.partial = static_cast<float*>(take(gemm_part > attn_part ? gemm_part : attn_part));
   w.counters = static_cast<int32_t*>(take(tiles * sizeof(int32_t)));
@@ -389,7 +389,7 @@ fd_status fd_block_forward(const fd_plan* plan, const fd_dims* dims, const fd_bl
                                     fdh::gemm_max_tiles(), s));
   fdh::GemmArgs g{};
   g.n_max = N; g.m = m; g.idx = idx; g.cu_q = cu_q; g.n_req = B; g.D = D;
-  g.partial = bw.partial; g.counters = bw.counters; g.max_units = fdh::gemm_max_tiles();
+  g.partial = bw.partial; g.max_units = fdh::gemm_max_tiles();
   g.act = bw.a; g.wt = w->w_qkv; g.bias = w->b_qkv; g.N = 3 * D; g.K = D;
   g.out_bf16 = bw.q; g.k_cache = k_cache; g.v_cache = v_cache;
   FD_LAUNCH(FD_K_GEMM_QKV, s, fdh::launch_gemm(fdh::GEMM_QKV, g, s));
@@ -398,19 +398,19 @@ fd_status fd_block_forward(const fd_plan* plan, const fd_dims* dims, const fd_bl
                                   plan->max_request_tokens, bw.partial, bw.counters, bw.lse, s));
   g = fdh::GemmArgs{};
   g.n_max = N; g.m = m; g.idx = idx; g.cu_q = cu_q; g.n_req = B; g.D = D;
-  g.partial = bw.partial; g.counters = bw.counters; g.max_units = fdh::gemm_max_tiles();
+  g.partial = bw.partial; g.max_units = fdh::gemm_max_tiles();
   g.act = bw.o; g.wt = w->w_o; g.bias = w->b_o; g.N = D; g.K = D;
   g.out_f32 = h; g.gate = mod + 2 * D; g.gate_stride = 6 * D;
   FD_LAUNCH(FD_K_GEMM_O, s, fdh::launch_gemm(fdh::GEMM_RESID, g, s));
   FD_LAUNCH(FD_K_LN, s, fdh::launch_ln_modulate(h, cu_q, B, m, N, D, mod, 6 * D, 3 * D, 4 * D, bw.a, nullptr, 0, s));
   g = fdh::GemmArgs{};
   g.n_max = N; g.m = m; g.idx = idx; g.cu_q = cu_q; g.n_req = B; g.D = D;
-  g.partial = bw.partial; g.counters = bw.counters; g.max_units = fdh::gemm_max_tiles();
+  g.partial = bw.partial; g.max_units = fdh::gemm_max_tiles();
   g.act = bw.a; g.wt = w->w_1; g.bias = w->b_1; g.N = F; g.K = D; g.out_bf16 = bw.g;
   FD_LAUNCH(FD_K_GEMM_MLP1, s, fdh::launch_gemm(fdh::GEMM_GELU, g, s));
   g = fdh::GemmArgs{};
   g.n_max = N; g.m = m; g.idx = idx; g.cu_q = cu_q; g.n_req = B; g.D = D;
-  g.partial = bw.partial; g.counters = bw.counters; g.max_units = fdh::gemm_max_tiles();
+  g.partial = bw.partial; g.max_units = fdh::gemm_max_tiles();
   g.act = bw.g; g.wt = w->w_2; g.bias = w->b_2; g.N = D; g.K = F;
   g.out_f32 = h; g.gate = mod + 5 * D; g.gate_stride = 6 * D;
   FD_LAUNCH(FD_K_GEMM_MLP2, s, fdh::launch_gemm(fdh::GEMM_RESID, g, s));
@@ -497,7 +497,7 @@ fd_status fd_final(const fd_plan* plan, const fd_dims* dims, const fd_final_weig
   FD_LAUNCH(FD_K_LN, s, fdh::launch_ln_modulate(h, cu_q, B, m, N, D, bw.mod, 2 * D, 0, D, bw.a, nullptr, 0, s));
   fdh::GemmArgs g{};
   g.n_max = N; g.m = m; g.cu_q = cu_q; g.n_req = B;
-  g.partial = bw.partial; g.counters = bw.counters; g.max_units = fdh::gemm_max_tiles();
+  g.partial = bw.partial; g.max_units = fdh::gemm_max_tiles();
   g.act = bw.a; g.wt = w->w_out; g.bias = w->b_out; g.N = dims->C; g.K = D; g.out_f32 = v;
   FD_LAUNCH(FD_K_FINAL, s, fdh::launch_gemm(fdh::GEMM_OUT, g, s));
   return FD_OK;

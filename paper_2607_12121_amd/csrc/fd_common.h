@@ -127,10 +127,10 @@ struct GemmArgs {
   float* out_f32;        // RESID: h [M][N] (+=); EMBED: h [M][N]; OUT: v [M][N]
   const float* gate; int gate_stride;          // RESID: gate row per request
   const float* pos;      // EMBED: [N_tok][N]
-  // split-K scratch (tiled kernel): fp32 partial tiles and per-tile arrival counters
-  float* partial; int32_t* counters; int max_units;
+  // split-K scratch (tiled kernel): fp32 partial tiles, summed by a second kernel
+  float* partial; int max_units;
 };
-// Bytes of split-K scratch the tiled GEMM needs (partials + counters), for any shape.
+// Bytes of split-K scratch the tiled GEMM needs (fp32 partial tiles), for any shape.
 size_t gemm_scratch_bytes();
 int gemm_max_tiles();
 hipError_t launch_gemm(GemmKind kind, const GemmArgs& a, hipStream_t s);

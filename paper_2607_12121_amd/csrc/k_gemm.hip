@@ -20,14 +20,17 @@
 // past M (or N) re-read the last valid row; their results are never stored.
 //
 // Split-K (128x128 tiles only, when the tile count leaves CUs idle and K is long):
-// every tile's K range is cut into S contiguous splits.  Each split stores its fp32
-// tile to scratch and bumps the tile's arrival counter; the last split to arrive
-// sums all S partials in split order (deterministic), runs the epilogue and
-// resets the counter for the next launch.
+// every tile's K range is cut into S contiguous splits, each storing its fp32 tile
+// to scratch; a second kernel sums the S partials in split order (deterministic)
+// and runs the epilogue.  No workgroup waits for another: the kernel boundary
+// orders the partial stores before the sums.
 //
-// Epilogue: each wave moves one 32x32 accumulator block at a time through a
-// private LDS patch and finishes 16 consecutive columns of one row per lane with
-// vector loads and stores.
+// The MFMA takes the weight fragment as its first operand, so each accumulator
+// block is the transposed output block: a lane holds one output row and four runs
+// of four consecutive columns.  The epilogue works from those registers (no LDS):
+// fp32 outputs as float4, bf16 outputs as 16-byte runs after exchanging halves
+// between lanes l and l + 32; per-row operands (token, request) are loaded before
+// the K loop, and the gated residual keeps the next block's loads in flight.
 //
 // Work units are dealt to the 8 XCDs in contiguous chunks of tile order (a WG
 // runs on XCD blockIdx.x % 8), so the tiles one XCD runs concurrently share A
@@ -65,61 +68,67 @@ FD_DEVICE void epilogue(const fdh::GemmArgs& g, int row, int col, float acc) {
   }
 }
 
-// Epilogue on 8 consecutive columns col..col+7 of one output row (col % 8 == 0,
-// col + 8 <= N): v holds the fp32 accumulators.  Vector loads and stores only.
+// Epilogue of one 32x32 output block held transposed in a wave's accumulator (the
+// MFMA takes the weight fragment as its first operand): lane (l32, lg) holds output
+// row `row` and, in registers 4q .. 4q+3, columns c_q = cb + 8q + 4lg .. +3.  Every
+// lane runs it (the bf16 kinds exchange halves between lanes l and l + 32); rows
+// past M and columns past N (N % 16 == 0) are not stored.  tok: the row's token
+// (QKV, EMBED).  RESID has its own pipelined loop in the caller.
 template <int KIND>
-FD_DEVICE void epilogue8(const fdh::GemmArgs& g, int row, int col, float v[8]) {
-  const float4 b0 = *reinterpret_cast<const float4*>(g.bias + col);
-  const float4 b1 = *reinterpret_cast<const float4*>(g.bias + col + 4);
-  v[0] += b0.x; v[1] += b0.y; v[2] += b0.z; v[3] += b0.w;
-  v[4] += b1.x; v[5] += b1.y; v[6] += b1.z; v[7] += b1.w;
+FD_DEVICE void epilogue_block(const fdh::GemmArgs& g, bool row_ok, int row, int cb, int lg, int tok, const f32x16_t& acc) {
+  const int N = g.N;
+  float v[16];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const float4 b = *reinterpret_cast<const float4*>(g.bias + min(cb + 8 * q + 4 * lg, N - 4));
+    v[4 * q + 0] = acc[4 * q + 0] + b.x;
+    v[4 * q + 1] = acc[4 * q + 1] + b.y;
+    v[4 * q + 2] = acc[4 * q + 2] + b.z;
+    v[4 * q + 3] = acc[4 * q + 3] + b.w;
+  }
   if constexpr (KIND == fdh::GEMM_QKV || KIND == fdh::GEMM_GELU) {
     if constexpr (KIND == fdh::GEMM_GELU) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] = fd::gelu_tanh_fast(v[e]);
+      for (int e = 0; e < 16; ++e) v[e] = fd::gelu_tanh_fast(v[e]);
     }
-    uint4 o;
-    o.x = fd::pack_bf2(v[0], v[1]);
-    o.y = fd::pack_bf2(v[2], v[3]);
-    o.z = fd::pack_bf2(v[4], v[5]);
-    o.w = fd::pack_bf2(v[6], v[7]);
-    uint16_t* dst;
+    uint32_t pk[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) pk[e] = fd::pack_bf2(v[2 * e], v[2 * e + 1]);
+    uint16_t* base;
+    int c0 = cb;
     if constexpr (KIND == fdh::GEMM_QKV) {
       const int D = g.D;
-      if (col < D) {
-        dst = g.out_bf16 + static_cast<size_t>(row) * D + col;
+      if (cb < D) {
+        base = g.out_bf16 + static_cast<size_t>(row) * D;
       } else {
-        const size_t tok = static_cast<size_t>(g.idx[row]);
-        dst = (col < 2 * D) ? g.k_cache + tok * D + (col - D) : g.v_cache + tok * D + (col - 2 * D);
+        base = (cb < 2 * D ? g.k_cache : g.v_cache) + static_cast<size_t>(tok) * D;
+        c0 = cb - (cb < 2 * D ? D : 2 * D);
       }
     } else {
-      dst = g.out_bf16 + static_cast<size_t>(row) * g.N + col;
+      base = g.out_bf16 + static_cast<size_t>(row) * N;
     }
-    *reinterpret_cast<uint4*>(dst) = o;
+#pragma unroll
+    for (int p = 0; p < 2; ++p) {
+      // lanes 0-31 gather columns 16p .. 16p+7 of the block, lanes 32-63 16p+8 .. 16p+15
+      const auto lo = __builtin_amdgcn_permlane32_swap(pk[4 * p + 0], pk[4 * p + 2], false, false);
+      const auto hi = __builtin_amdgcn_permlane32_swap(pk[4 * p + 1], pk[4 * p + 3], false, false);
+      const uint4 o = make_uint4(lo[0], hi[0], lo[1], hi[1]);
+      const int off = 16 * p + 8 * lg;
+      if (row_ok && cb + off < N) *reinterpret_cast<uint4*>(base + c0 + off) = o;
+    }
   } else {
-    float* hp = g.out_f32 + static_cast<size_t>(row) * g.N + col;
-    float4 r0, r1;
-    if constexpr (KIND == fdh::GEMM_RESID) {
-      const int b = fd::row_request(g.cu_q, g.n_req, row);
-      const float* gp = g.gate + static_cast<size_t>(b) * g.gate_stride + col;
-      const float4 g0 = *reinterpret_cast<const float4*>(gp);
-      const float4 g1 = *reinterpret_cast<const float4*>(gp + 4);
-      const float4 h0 = *reinterpret_cast<const float4*>(hp);
-      const float4 h1 = *reinterpret_cast<const float4*>(hp + 4);
-      r0 = make_float4(h0.x + g0.x * v[0], h0.y + g0.y * v[1], h0.z + g0.z * v[2], h0.w + g0.w * v[3]);
-      r1 = make_float4(h1.x + g1.x * v[4], h1.y + g1.y * v[5], h1.z + g1.z * v[6], h1.w + g1.w * v[7]);
-    } else if constexpr (KIND == fdh::GEMM_EMBED) {
-      const float* pp = g.pos + static_cast<size_t>(g.idx[row]) * g.N + col;
-      const float4 p0 = *reinterpret_cast<const float4*>(pp);
-      const float4 p1 = *reinterpret_cast<const float4*>(pp + 4);
-      r0 = make_float4(v[0] + p0.x, v[1] + p0.y, v[2] + p0.z, v[3] + p0.w);
-      r1 = make_float4(v[4] + p1.x, v[5] + p1.y, v[6] + p1.z, v[7] + p1.w);
-    } else {
-      r0 = make_float4(v[0], v[1], v[2], v[3]);
-      r1 = make_float4(v[4], v[5], v[6], v[7]);
+    float* out = g.out_f32 + static_cast<size_t>(row) * N;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int c = cb + 8 * q + 4 * lg;
+      if (!row_ok || c >= N) continue;
+      float4 r = make_float4(v[4 * q], v[4 * q + 1], v[4 * q + 2], v[4 * q + 3]);
+      if constexpr (KIND == fdh::GEMM_EMBED) {
+        const float4 pp = *reinterpret_cast<const float4*>(g.pos + static_cast<size_t>(tok) * N + c);
+        r.x += pp.x; r.y += pp.y; r.z += pp.z; r.w += pp.w;
+      }
+      *reinterpret_cast<float4*>(out + c) = r;
     }
-    reinterpret_cast<float4*>(hp)[0] = r0;
-    reinterpret_cast<float4*>(hp)[1] = r1;
   }
 }
 
@@ -162,6 +171,7 @@ static_assert(kSmallRing >= CfgSmall::STAGES * CfgSmall::CHUNKS + 1 && kSmallRin
 
 constexpr int TBK = 64;
 constexpr int kMaxSplit = 16;
+constexpr int kMinSplitSteps = 24;   // K-steps every split keeps
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 typedef int int32x4_t __attribute__((ext_vector_type(4)));
@@ -199,18 +209,77 @@ FD_DEVICE void wait_vm_barrier() {
 // at least 24 K-steps and the units still fit the resident workgroup slots.
 FD_DEVICE int choose_split(int tiles, int nk, int slots, int max_units) {
   int s = 1;
-  while (s < kMaxSplit && tiles * (s + 1) <= slots && tiles * (s + 1) <= max_units && nk / (s + 1) >= 24) ++s;
+  while (s < kMaxSplit && tiles * (s + 1) <= slots && tiles * (s + 1) <= max_units && nk / (s + 1) >= kMinSplitSteps) ++s;
   return s;
 }
 
+// Epilogue of a wave's FM x FN accumulator blocks, straight from the registers:
+// acc[i][j] is the transposed 32x32 block at rows row0 + 32i, columns cw + 32j (see
+// epilogue_block); rtok / rreq are the token / request of row row0 + 32i.
+template <int FM, int FN, int KIND>
+FD_DEVICE void tile_epilogue(const fdh::GemmArgs& g, int M, int row0, int cw, int lg, const int (&rtok)[FM],
+                             const int (&rreq)[FM], const f32x16_t (&acc)[FM][FN]) {
+  const int N = g.N;
+  if constexpr (KIND == fdh::GEMM_RESID) {
+    // h += gate * (acc + bias): the next block's h and gate rows are loaded before
+    // this block's stores, so each wave keeps two blocks of loads in flight
+    constexpr int NB = FM * FN;
+    float4 hb[2][4], gb[2][4];
+    auto load_blk = [&](int bi, int sl) {
+      const int i = bi / FN, j = bi - (bi / FN) * FN;
+      const int r = min(row0 + 32 * i, M - 1);
+      const float* hp = g.out_f32 + static_cast<size_t>(r) * N;
+      const float* gp = g.gate + static_cast<size_t>(rreq[i]) * g.gate_stride;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int c = min(cw + 32 * j + 8 * q + 4 * lg, N - 4);
+        hb[sl][q] = *reinterpret_cast<const float4*>(hp + c);
+        gb[sl][q] = *reinterpret_cast<const float4*>(gp + c);
+      }
+    };
+    load_blk(0, 0);
+#pragma unroll
+    for (int bi = 0; bi < NB; ++bi) {
+      if (bi + 1 < NB) load_blk(bi + 1, (bi + 1) & 1);
+      const int i = bi / FN, j = bi - (bi / FN) * FN, sl = bi & 1;
+      const int row = row0 + 32 * i;
+      float* hp = g.out_f32 + static_cast<size_t>(row) * N;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int c = cw + 32 * j + 8 * q + 4 * lg;
+        const float4 bs = *reinterpret_cast<const float4*>(g.bias + min(c, N - 4));
+        const float4 h4 = hb[sl][q], g4 = gb[sl][q];
+        const float4 r4 = make_float4(h4.x + g4.x * (acc[i][j][4 * q + 0] + bs.x), h4.y + g4.y * (acc[i][j][4 * q + 1] + bs.y),
+                                      h4.z + g4.z * (acc[i][j][4 * q + 2] + bs.z), h4.w + g4.w * (acc[i][j][4 * q + 3] + bs.w));
+        if (row < M && c < N) *reinterpret_cast<float4*>(hp + c) = r4;
+      }
+    }
+  } else {
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        epilogue_block<KIND>(g, row0 + 32 * i < M, row0 + 32 * i, cw + 32 * j, lg, rtok[i], acc[i][j]);
+  }
+}
+
+// Token and request of this lane's output rows row0 + 32i (clamped to M - 1).
+template <int FM, int KIND>
+FD_DEVICE void row_operands(const fdh::GemmArgs& g, int M, int row0, int (&rtok)[FM], int (&rreq)[FM]) {
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+    const int r = min(row0 + 32 * i, M - 1);
+    rtok[i] = (KIND == fdh::GEMM_QKV || KIND == fdh::GEMM_EMBED) ? g.idx[r] : 0;
+    rreq[i] = (KIND == fdh::GEMM_RESID) ? fd::row_request(g.cu_q, g.n_req, r) : 0;
+  }
+}
+
 // All tiles of one GEMM with tile shape Cfg, the workgroup's LDS ring at ring_mem
-// (STAGES * CHUNKS 16-byte chunks at least) and the split-K arrival flag at s_last.
+// (STAGES * CHUNKS 16-byte chunks at least).
 template <class Cfg, int KIND>
-FD_DEVICE void gemm_tiles(const fdh::GemmArgs& g, int slots, int M, uint4* ring_mem, int& s_last) {
+FD_DEVICE void gemm_tiles(const fdh::GemmArgs& g, int slots, int M, uint4* ring_mem) {
   constexpr int BM = Cfg::BM, BN = Cfg::BN, FM = Cfg::FM, FN = Cfg::FN, TM = Cfg::TM, TN = Cfg::TN;
   constexpr int WAVES = Cfg::WAVES, THREADS = Cfg::THREADS, LOADS = Cfg::LOADS, STAGES = Cfg::STAGES;
-  constexpr int PATCH = 32 * 36;   // per-wave epilogue patch (floats), row stride 36
-  static_assert(WAVES * PATCH * 4 <= STAGES * Cfg::CHUNKS * 16, "epilogue patches must fit in the ring");
   const int N = g.N, K = g.K;
   const int tiles_m = (M + BM - 1) / BM;
   const int tiles_n = (N + BN - 1) / BN;
@@ -273,6 +342,12 @@ FD_DEVICE void gemm_tiles(const fdh::GemmArgs& g, int slots, int M, uint4* ring_
     };
     auto issue = [&](int kt, int st) { issue_q(kt, st, 0, LOADS); };
 
+    // this lane's output rows (one per 32-row block) and their token / request,
+    // loaded before the K loop so that the epilogue never waits on them
+    const int row0 = m0 + wm * TM + l32;
+    int rtok[FM], rreq[FM];
+    row_operands<FM, KIND>(g, M, row0, rtok, rreq);
+
     f32x16_t acc[FM][FN];
 #pragma unroll
     for (int i = 0; i < FM; ++i)
@@ -316,7 +391,7 @@ FD_DEVICE void gemm_tiles(const fdh::GemmArgs& g, int slots, int M, uint4* ring_
         for (int i = 0; i < FM; ++i)
 #pragma unroll
           for (int j = 0; j < FN; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[ks & 1][i], b[ks & 1][j], acc[i][j], 0, 0, 0);
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(b[ks & 1][j], a[ks & 1][i], acc[i][j], 0, 0, 0);
       }
       // schedule: first fragments, then per k16 step one next-step read after each of
       // the first FM + FN MFMAs, then the remaining MFMAs
@@ -337,80 +412,21 @@ FD_DEVICE void gemm_tiles(const fdh::GemmArgs& g, int slots, int M, uint4* ring_
     __syncthreads();
 
     if (S > 1) {
-      // Store this split's tile (lane-major: element e of thread t at e * THREADS + t)
-      // with device-coherent stores; once the workgroup's stores are done, thread 0
-      // counts the arrival with a release read-modify-write at agent scope, and the
-      // last split to arrive acquires before it reads the partials (the splits may
-      // have run on other XCDs).
-      float* slot = g.partial + static_cast<size_t>(v) * (BM * BN) + tid;
+      // Store this split's fp32 tile for splitk_reduce_kernel (float4 r4 of block
+      // (i, j) of thread t at float4 index ((i * FN + j) * 4 + r4) * THREADS + t).
+      f32x4_t* slot = reinterpret_cast<f32x4_t*>(g.partial + static_cast<size_t>(v) * (BM * BN)) + tid;
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
         for (int j = 0; j < FN; ++j)
 #pragma unroll
-          for (int r = 0; r < 16; ++r)
-            __hip_atomic_store(slot + ((i * FN + j) * 16 + r) * THREADS, acc[i][j][r], __ATOMIC_RELAXED,
-                               __HIP_MEMORY_SCOPE_AGENT);
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this wave's partials have been performed
-      __syncthreads();   // ... and happen before thread 0's release below (workgroup barrier)
-      if (tid == 0) {
-        const int prev = __hip_atomic_fetch_add(&g.counters[tile], 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-        if (prev == S - 1) {
-          // the last arrival: acquire every split's released partials, reset the counter
-          __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-          __hip_atomic_store(&g.counters[tile], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
-        s_last = (prev == S - 1);
-      }
-      __syncthreads();   // thread 0's acquire happens before every thread's loads below
-      if (!s_last) continue;
-      // Sum the S partials (this split's included) in split order with
-      // device-coherent loads: the result does not depend on which split arrived last.
-      const float* base = g.partial + static_cast<size_t>(tile) * S * (BM * BN) + tid;
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-#pragma unroll
-          for (int r = 0; r < 16; ++r)
-            acc[i][j][r] = __hip_atomic_load(base + ((i * FN + j) * 16 + r) * THREADS, __ATOMIC_RELAXED,
-                                             __HIP_MEMORY_SCOPE_AGENT);
-      for (int s2 = 1; s2 < S; ++s2) {
-        const float* ps = base + static_cast<size_t>(s2) * (BM * BN);
-#pragma unroll
-        for (int i = 0; i < FM; ++i)
-#pragma unroll
-          for (int j = 0; j < FN; ++j)
-#pragma unroll
-            for (int r = 0; r < 16; ++r)
-              acc[i][j][r] += __hip_atomic_load(ps + ((i * FN + j) * 16 + r) * THREADS, __ATOMIC_RELAXED,
-                                                __HIP_MEMORY_SCOPE_AGENT);
-      }
+          for (int r4 = 0; r4 < 4; ++r4)
+            slot[((i * FN + j) * 4 + r4) * THREADS] =
+                f32x4_t{acc[i][j][4 * r4], acc[i][j][4 * r4 + 1], acc[i][j][4 * r4 + 2], acc[i][j][4 * r4 + 3]};
+      continue;
     }
 
-    // Epilogue, one 32x32 block at a time through this wave's LDS patch
-    // (accumulator layout: lane holds column l32, rows 8*(r/4) + 4*lg + (r%4));
-    // lane then owns row lane/2, columns 16*(lane%2) .. +15 of the block.
-    float* patch = reinterpret_cast<float*>(ring_mem) + wave * PATCH;
-    const int pr = lane >> 1, pc = (lane & 1) * 16;
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-      for (int j = 0; j < FN; ++j) {
-#pragma unroll
-        for (int r = 0; r < 16; ++r) patch[(8 * (r >> 2) + 4 * lg + (r & 3)) * 36 + l32] = acc[i][j][r];
-        const int row = m0 + wm * TM + i * 32 + pr, col = n0 + wn * TN + j * 32 + pc;
-        const float4* src = reinterpret_cast<const float4*>(patch + pr * 36 + pc);
-        float v0[8], v1[8];
-        const float4 x0 = src[0], x1 = src[1], x2 = src[2], x3 = src[3];
-        v0[0] = x0.x; v0[1] = x0.y; v0[2] = x0.z; v0[3] = x0.w; v0[4] = x1.x; v0[5] = x1.y; v0[6] = x1.z; v0[7] = x1.w;
-        v1[0] = x2.x; v1[1] = x2.y; v1[2] = x2.z; v1[3] = x2.w; v1[4] = x3.x; v1[5] = x3.y; v1[6] = x3.z; v1[7] = x3.w;
-        if (row < M) {
-          if (col < N) epilogue8<KIND>(g, row, col, v0);
-          if (col + 8 < N) epilogue8<KIND>(g, row, col + 8, v1);
-        }
-      }
-    __syncthreads();   // the patches are the next unit's ring
+    tile_epilogue<FM, FN, KIND>(g, M, row0, n0 + wn * TN, lg, rtok, rreq, acc);
   }
 }
 
@@ -436,23 +452,70 @@ FD_DEVICE int small_shape(int M, int N, int K, int slots, int max_units) {
 template <int KIND>
 __global__ __launch_bounds__(256, 2) void gemm_small_kernel(fdh::GemmArgs g, int slots) {
   __shared__ uint4 ring_mem[kSmallRing];
-  int& s_last = *reinterpret_cast<int*>(&ring_mem[kSmallRing - 1]);   // outside the 128x128 ring
   const int M = min(*g.m, g.n_max);
   if (M <= 0) return;
   switch (small_shape(M, g.N, g.K, slots, g.max_units)) {
-    case 1: gemm_tiles<CfgWide, KIND>(g, slots, M, ring_mem, s_last); break;
-    case 2: gemm_tiles<CfgNarrow, KIND>(g, slots, M, ring_mem, s_last); break;
-    default: gemm_tiles<CfgSmall, KIND>(g, slots, M, ring_mem, s_last); break;
+    case 1: gemm_tiles<CfgWide, KIND>(g, slots, M, ring_mem); break;
+    case 2: gemm_tiles<CfgNarrow, KIND>(g, slots, M, ring_mem); break;
+    default: gemm_tiles<CfgSmall, KIND>(g, slots, M, ring_mem); break;
   }
 }
 
 template <int KIND>
 __global__ __launch_bounds__(CfgLarge::THREADS, CfgLarge::OCC) void gemm_large_kernel(fdh::GemmArgs g, int slots) {
   __shared__ uint4 ring_mem[CfgLarge::STAGES * CfgLarge::CHUNKS];
-  __shared__ int s_last;
   const int M = min(*g.m, g.n_max);
   if (M <= 0) return;
-  gemm_tiles<CfgLarge, KIND>(g, slots, M, ring_mem, s_last);
+  gemm_tiles<CfgLarge, KIND>(g, slots, M, ring_mem);
+}
+
+// Split-K reduction: when the GEMM above split its 128x128 tiles (same M, shape and
+// split count, recomputed here), the S partial tiles are summed in split order
+// (deterministic) and the epilogue runs with the GEMM's thread geometry, one
+// workgroup per (tile, 32x32 block of every wave): four per tile, so that each
+// thread keeps all of its S partial loads in flight.  The kernel boundary orders
+// the partial stores before these loads.
+template <int KIND>
+__global__ __launch_bounds__(CfgSmall::THREADS) void splitk_reduce_kernel(fdh::GemmArgs g, int slots) {
+  using Cfg = CfgSmall;
+  constexpr int FM = Cfg::FM, FN = Cfg::FN, NB = FM * FN, THREADS = Cfg::THREADS;
+  const int M = min(*g.m, g.n_max);
+  if (M <= 0) return;
+  const int tiles_m = (M + Cfg::BM - 1) / Cfg::BM, tiles_n = (g.N + Cfg::BN - 1) / Cfg::BN;
+  const int tiles = tiles_m * tiles_n;
+  const int S = choose_split(tiles, g.K / TBK, slots, g.max_units);
+  if (S == 1) return;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave / Cfg::WN, wn = wave % Cfg::WN, l32 = lane & 31, lg = lane >> 5;
+  for (int w = blockIdx.x; w < tiles * NB; w += gridDim.x) {
+    const int tile = w / NB, bi = w - tile * NB, i = bi / FN, j = bi - (bi / FN) * FN;
+    const int m0 = (tile % tiles_m) * Cfg::BM, n0 = (tile / tiles_m) * Cfg::BN;
+    const int row0 = m0 + wm * Cfg::TM + 32 * i + l32;
+    int rtok[1], rreq[1];
+    row_operands<1, KIND>(g, M, row0, rtok, rreq);
+    const f32x4_t* base = reinterpret_cast<const f32x4_t*>(g.partial + static_cast<size_t>(tile) * S * kSmallTile) +
+                          static_cast<size_t>(bi * 4) * THREADS + tid;
+    f32x16_t acc[1][1];
+#pragma unroll
+    for (int e = 0; e < 16; ++e) acc[0][0][e] = 0.f;
+    // four splits' loads at a time, summed in split order (the first add is onto 0)
+    for (int s0 = 0; s0 < S; s0 += 4) {
+      f32x4_t p[4][4];
+#pragma unroll
+      for (int sp = 0; sp < 4; ++sp)
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4)
+          p[sp][r4] = (s0 + sp < S) ? base[static_cast<size_t>(s0 + sp) * (kSmallTile / 4) + r4 * THREADS] : f32x4_t{};
+#pragma unroll
+      for (int sp = 0; sp < 4; ++sp)
+        if (s0 + sp < S) {
+#pragma unroll
+          for (int r4 = 0; r4 < 4; ++r4)
+            for (int e = 0; e < 4; ++e) acc[0][0][4 * r4 + e] += p[sp][r4][e];
+        }
+    }
+    tile_epilogue<1, 1, KIND>(g, M, row0, n0 + wn * Cfg::TN + 32 * j, lg, rtok, rreq, acc);
+  }
 }
 
 // ---------------------------------------------------------------- simple kernel (any K % 8 == 0)
@@ -574,7 +637,7 @@ int gemm_max_tiles() { return 4 * num_cus(); }
 
 size_t gemm_scratch_bytes() {
   const size_t units = static_cast<size_t>(gemm_max_tiles());
-  return units * kSmallTile * sizeof(float) + units * sizeof(int32_t);
+  return units * kSmallTile * sizeof(float);
 }
 
 namespace {
@@ -601,6 +664,11 @@ hipError_t launch_tiled(GemmKind kind, const GemmArgs& a, int max_units, bool la
     gemm_large_kernel<K><<<grid, CfgLarge::THREADS, 0, s>>>(g, slots);                         \
   else                                                                                         \
     gemm_small_kernel<K><<<grid, 256, 0, s>>>(g, slots);
+  // the split-K reduction, launched whenever K is long enough for a split (it
+  // returns at once when the device-side M gave S = 1)
+  const bool may_split = !large && max_units > 0 && (a.K / TBK) >= 2 * kMinSplitSteps;
+  const long long red_units = static_cast<long long>((a.n_max + 127) / 128) * ((a.N + 127) / 128) * CfgSmall::FM * CfgSmall::FN;
+  const int red_grid = static_cast<int>(red_units < 4 * slots ? red_units : 4 * slots);
   switch (kind) {
     case GEMM_QKV: FD_GEMM_LAUNCH(GEMM_QKV) break;
     case GEMM_RESID: FD_GEMM_LAUNCH(GEMM_RESID) break;
@@ -609,13 +677,22 @@ hipError_t launch_tiled(GemmKind kind, const GemmArgs& a, int max_units, bool la
     case GEMM_OUT: FD_GEMM_LAUNCH(GEMM_OUT) break;
   }
 #undef FD_GEMM_LAUNCH
+  if (may_split) {
+    switch (kind) {
+      case GEMM_QKV: splitk_reduce_kernel<GEMM_QKV><<<red_grid, CfgSmall::THREADS, 0, s>>>(g, slots); break;
+      case GEMM_RESID: splitk_reduce_kernel<GEMM_RESID><<<red_grid, CfgSmall::THREADS, 0, s>>>(g, slots); break;
+      case GEMM_GELU: splitk_reduce_kernel<GEMM_GELU><<<red_grid, CfgSmall::THREADS, 0, s>>>(g, slots); break;
+      case GEMM_EMBED: splitk_reduce_kernel<GEMM_EMBED><<<red_grid, CfgSmall::THREADS, 0, s>>>(g, slots); break;
+      case GEMM_OUT: splitk_reduce_kernel<GEMM_OUT><<<red_grid, CfgSmall::THREADS, 0, s>>>(g, slots); break;
+    }
+  }
   return hipGetLastError();
 }
 }  // namespace
 
 hipError_t launch_gemm(GemmKind kind, const GemmArgs& a, hipStream_t s) {
   if (a.K % TBK == 0) {
-    const int max_units = (a.partial && a.counters) ? a.max_units : 0;   // no scratch: never split
+    const int max_units = a.partial ? a.max_units : 0;   // no scratch: never split
     if (a.n_max >= kLargeTileRows && a.N >= 1024) return launch_tiled(kind, a, 0, true, s);
     return launch_tiled(kind, a, max_units, false, s);
   }
