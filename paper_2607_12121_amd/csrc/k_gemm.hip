@@ -72,19 +72,24 @@ FD_DEVICE void epilogue(const fdh::GemmArgs& g, int row, int col, float acc) {
 // MFMA takes the weight fragment as its first operand): lane (l32, lg) holds output
 // row `row` and, in registers 4q .. 4q+3, columns c_q = cb + 8q + 4lg .. +3.  Every
 // lane runs it (the bf16 kinds exchange halves between lanes l and l + 32); rows
-// past M and columns past N (N % 16 == 0) are not stored.  tok: the row's token
-// (QKV, EMBED).  RESID has its own pipelined loop in the caller.
-template <int KIND>
-FD_DEVICE void epilogue_block(const fdh::GemmArgs& g, bool row_ok, int row, int cb, int lg, int tok, const f32x16_t& acc) {
+// past M and columns past N (N % 16 == 0) are not stored (with kAlwaysStore, the
+// bf16 kinds issue every store and send those lanes' data to `spare`).  The
+// accumulators started at the bias, or at 0 with the block's 32 bias values at
+// lds_bias.  tok: the row's token (QKV, EMBED).  RESID has its own pipelined loop
+// in the caller.
+template <int KIND, bool kAlwaysStore = false>
+FD_DEVICE void epilogue_block(const fdh::GemmArgs& g, bool row_ok, int row, int cb, int lg, int tok, const f32x16_t& acc,
+                              float4* spare = nullptr, const float* lds_bias = nullptr) {
   const int N = g.N;
   float v[16];
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const float4 b = *reinterpret_cast<const float4*>(g.bias + min(cb + 8 * q + 4 * lg, N - 4));
-    v[4 * q + 0] = acc[4 * q + 0] + b.x;
-    v[4 * q + 1] = acc[4 * q + 1] + b.y;
-    v[4 * q + 2] = acc[4 * q + 2] + b.z;
-    v[4 * q + 3] = acc[4 * q + 3] + b.w;
+  for (int e = 0; e < 16; ++e) v[e] = acc[e];
+  if (lds_bias) {   // the bias of the block's columns from LDS (the accumulators started at 0)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float4 b = *reinterpret_cast<const float4*>(lds_bias + 8 * q + 4 * lg);
+      v[4 * q + 0] += b.x; v[4 * q + 1] += b.y; v[4 * q + 2] += b.z; v[4 * q + 3] += b.w;
+    }
   }
   if constexpr (KIND == fdh::GEMM_QKV || KIND == fdh::GEMM_GELU) {
     if constexpr (KIND == fdh::GEMM_GELU) {
@@ -114,7 +119,13 @@ FD_DEVICE void epilogue_block(const fdh::GemmArgs& g, bool row_ok, int row, int 
       const auto hi = __builtin_amdgcn_permlane32_swap(pk[4 * p + 1], pk[4 * p + 3], false, false);
       const uint4 o = make_uint4(lo[0], hi[0], lo[1], hi[1]);
       const int off = 16 * p + 8 * lg;
-      if (row_ok && cb + off < N) *reinterpret_cast<uint4*>(base + c0 + off) = o;
+      if constexpr (kAlwaysStore) {
+        // one store instruction whatever the row: lanes past M or N write the spare slot
+        uint4* dst = (row_ok && cb + off < N) ? reinterpret_cast<uint4*>(base + c0 + off) : reinterpret_cast<uint4*>(spare);
+        *dst = o;
+      } else if (row_ok && cb + off < N) {
+        *reinterpret_cast<uint4*>(base + c0 + off) = o;
+      }
     }
   } else {
     float* out = g.out_f32 + static_cast<size_t>(row) * N;
@@ -164,6 +175,7 @@ using CfgWide = TileCfg<128, 192, 2, 2, 2, 2>;     // 1.5x the columns: one roun
 using CfgNarrow = TileCfg<128, 64, 2, 2, 3, 2>;
 using CfgLarge = TileCfg<256, 256, 2, 4, 2, 1, 64, false, 8>;   // tile order in groups of 8 row tiles
 constexpr int kSmallTile = 128 * 128;   // split-K partial tile (floats)
+constexpr int kSideChunks = 4 * 1024 / 16;   // two 1 KB bias slots and two 1 KB token slots (256x256 tile)
 // LDS ring of the two-workgroups-per-CU kernel: the largest of its three tile shapes
 constexpr int kSmallRing = CfgWide::STAGES * CfgWide::CHUNKS;
 static_assert(kSmallRing >= CfgSmall::STAGES * CfgSmall::CHUNKS + 1 && kSmallRing >= CfgNarrow::STAGES * CfgNarrow::CHUNKS,
@@ -176,13 +188,14 @@ constexpr int kMinSplitSteps = 24;   // K-steps every split keeps
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 typedef int int32x4_t __attribute__((ext_vector_type(4)));
 
-// Buffer resource of a raw byte buffer (base, no stride, 2^31-1 bytes in range).
-FD_DEVICE int32x4_t buffer_rsrc(const void* base) {
+// Buffer resource of a raw byte buffer (base, no stride, `bytes` in range: loads
+// past it return zeros).
+FD_DEVICE int32x4_t buffer_rsrc(const void* base, uint32_t bytes = 0x7fffffffu) {
   const uint64_t p = reinterpret_cast<uint64_t>(base);
   int32x4_t r;
   r.x = static_cast<int>(static_cast<uint32_t>(p));
   r.y = static_cast<int>(static_cast<uint32_t>(p >> 32) & 0xffffu);
-  r.z = 0x7fffffff;
+  r.z = static_cast<int>(bytes);
   r.w = 0x00020000;
   return r;
 }
@@ -221,7 +234,7 @@ FD_DEVICE void tile_epilogue(const fdh::GemmArgs& g, int M, int row0, int cw, in
                              const int (&rreq)[FM], const f32x16_t (&acc)[FM][FN]) {
   const int N = g.N;
   if constexpr (KIND == fdh::GEMM_RESID) {
-    // h += gate * (acc + bias): the next block's h and gate rows are loaded before
+    // h += gate * acc (the bias is in acc): the next block's h and gate rows are loaded before
     // this block's stores, so each wave keeps two blocks of loads in flight
     constexpr int NB = FM * FN;
     float4 hb[2][4], gb[2][4];
@@ -247,10 +260,9 @@ FD_DEVICE void tile_epilogue(const fdh::GemmArgs& g, int M, int row0, int cw, in
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int c = cw + 32 * j + 8 * q + 4 * lg;
-        const float4 bs = *reinterpret_cast<const float4*>(g.bias + min(c, N - 4));
         const float4 h4 = hb[sl][q], g4 = gb[sl][q];
-        const float4 r4 = make_float4(h4.x + g4.x * (acc[i][j][4 * q + 0] + bs.x), h4.y + g4.y * (acc[i][j][4 * q + 1] + bs.y),
-                                      h4.z + g4.z * (acc[i][j][4 * q + 2] + bs.z), h4.w + g4.w * (acc[i][j][4 * q + 3] + bs.w));
+        const float4 r4 = make_float4(h4.x + g4.x * acc[i][j][4 * q + 0], h4.y + g4.y * acc[i][j][4 * q + 1],
+                                      h4.z + g4.z * acc[i][j][4 * q + 2], h4.w + g4.w * acc[i][j][4 * q + 3]);
         if (row < M && c < N) *reinterpret_cast<float4*>(hp + c) = r4;
       }
     }
@@ -275,11 +287,22 @@ FD_DEVICE void row_operands(const fdh::GemmArgs& g, int M, int row0, int (&rtok)
 }
 
 // All tiles of one GEMM with tile shape Cfg, the workgroup's LDS ring at ring_mem
-// (STAGES * CHUNKS 16-byte chunks at least).
+// (STAGES * CHUNKS 16-byte chunks, followed by kSideChunks more for the bias and
+// token slots of the 256x256 bf16-output kinds).
+//
+// Units follow each other without a drain of the output stores: on the 256x256
+// tile with a bf16 output (QKV, GELU) the next unit's first stage, bias and row
+// tokens (copied into the LDS slots of the unit's parity) are issued before this
+// unit's epilogue, whose stores all issue (rows past M go to a spare slot), so the
+// next unit's first wait leaves exactly those stores in flight (vector memory
+// operations complete in issue order).  That path issues no other vector memory
+// operation the compiler would wait for.
 template <class Cfg, int KIND>
 FD_DEVICE void gemm_tiles(const fdh::GemmArgs& g, int slots, int M, uint4* ring_mem) {
   constexpr int BM = Cfg::BM, BN = Cfg::BN, FM = Cfg::FM, FN = Cfg::FN, TM = Cfg::TM, TN = Cfg::TN;
   constexpr int WAVES = Cfg::WAVES, THREADS = Cfg::THREADS, LOADS = Cfg::LOADS, STAGES = Cfg::STAGES;
+  constexpr bool kOverlap = BM * BN == 256 * 256 && (KIND == fdh::GEMM_QKV || KIND == fdh::GEMM_GELU);
+  constexpr int kEpiStores = 2 * FM * FN;   // stores of one unit's epilogue_block<KIND, true> calls
   const int N = g.N, K = g.K;
   const int tiles_m = (M + BM - 1) / BM;
   const int tiles_n = (N + BN - 1) / BN;
@@ -289,6 +312,8 @@ FD_DEVICE void gemm_tiles(const fdh::GemmArgs& g, int slots, int M, uint4* ring_
   const int S = (BM * BN == kSmallTile && g.max_units > 0) ? choose_split(tiles, nk, slots, g.max_units) : 1;
   const int units = tiles * S;
   const int per_xcd = (units + kXcds - 1) / kXcds;
+  constexpr bool overlap = kOverlap;   // g.partial (required) holds the spare slot of skipped stores
+  static_assert(!kOverlap || (BN == 256 && BM == 256), "one 16-byte copy per lane covers a slot");
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / Cfg::WN, wn = wave % Cfg::WN;
@@ -298,10 +323,15 @@ FD_DEVICE void gemm_tiles(const fdh::GemmArgs& g, int slots, int M, uint4* ring_
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);
   const uint32_t ring_base = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_ptr_t)&ring_mem[0]));
 
-  for (int u = blockIdx.x; u < per_xcd * kXcds; u += gridDim.x) {
-    const int v = (u % kXcds) * per_xcd + u / kXcds;
-    if (v >= units) continue;
-    const int tile = v / S, split = v - (v / S) * S;
+  // Work unit u of this workgroup (u = blockIdx.x, + gridDim.x, ...).  gridDim.x is
+  // a multiple of kXcds, so v grows with u and the valid units form a prefix.
+  struct Unit { int v, split, m0, n0, kt0, nkt; };
+  auto unit_at = [&](int u, Unit& t) -> bool {
+    if (u >= per_xcd * kXcds) return false;
+    t.v = (u % kXcds) * per_xcd + u / kXcds;
+    if (t.v >= units) return false;
+    const int tile = t.v / S;
+    t.split = t.v - tile * S;
     int tm, tn;
     if constexpr (Cfg::GROUP_M > 0) {
       // groups of GROUP_M row tiles x every column tile, row tile fastest: the tiles
@@ -316,54 +346,102 @@ FD_DEVICE void gemm_tiles(const fdh::GemmArgs& g, int slots, int M, uint4* ring_
       tm = tile % tiles_m;
       tn = tile / tiles_m;
     }
-    const int m0 = tm * BM, n0 = tn * BN;
-    const int kt0 = (split * nk) / S, kt1 = ((split + 1) * nk) / S;
-    const int nkt = kt1 - kt0;
-
-    // per-lane byte offsets (k = 0) of this lane's row and source chunk in each of its wave-loads
-    uint32_t off[LOADS];
+    t.m0 = tm * BM;
+    t.n0 = tn * BN;
+    t.kt0 = (t.split * nk) / S;
+    t.nkt = ((t.split + 1) * nk) / S - t.kt0;
+    return true;
+  };
+  // per-lane byte offsets (k = 0) of this lane's row and source chunk in each of its wave-loads
+  auto offsets = [&](const Unit& t, uint32_t (&o)[LOADS]) {
 #pragma unroll
     for (int q = 0; q < LOADS; ++q) {
       const int blk = wave + WAVES * q;        // 8-row block in the concatenated A|B tile
       const int r = blk * RPW + lane / CPR;
       const int c = (lane % CPR) ^ Cfg::swz(r);
-      const int gr = (q < Cfg::LOADS_A) ? min(m0 + r, M - 1) : min(n0 + (r - BM), N - 1);
-      off[q] = static_cast<uint32_t>((static_cast<size_t>(gr) * K + c * 8) * 2);   // chunk = 8 bf16
+      const int gr = (q < Cfg::LOADS_A) ? min(t.m0 + r, M - 1) : min(t.n0 + (r - BM), N - 1);
+      o[q] = static_cast<uint32_t>((static_cast<size_t>(gr) * K + c * 8) * 2);   // chunk = 8 bf16
     }
-    // wave-loads [q0, q1) of K-step kt into stage st
-    auto issue_q = [&](int kt, int st, int q0, int q1) {
-      const uint32_t buf = ring_base + static_cast<uint32_t>(st * Cfg::CHUNKS * 16);
-      const uint32_t kb = static_cast<uint32_t>((kt0 + kt) * BK * 2);
+  };
+  // wave-loads [q0, q1) of K-step kt of a unit (offsets o, first K-step kt0) into stage st
+  auto issue_q = [&](const uint32_t (&o)[LOADS], int kt0, int kt, int st, int q0, int q1) {
+    const uint32_t buf = ring_base + static_cast<uint32_t>(st * Cfg::CHUNKS * 16);
+    const uint32_t kb = static_cast<uint32_t>((kt0 + kt) * BK * 2);
 #pragma unroll
-      for (int q = 0; q < LOADS; ++q)
-        if (q >= q0 && q < q1)
-          lds_dma16(buf + static_cast<uint32_t>((wave_u + WAVES * q) * 64 * 16), off[q] + kb,
-                    q < Cfg::LOADS_A ? rs_a : rs_b);
-    };
-    auto issue = [&](int kt, int st) { issue_q(kt, st, 0, LOADS); };
+    for (int q = 0; q < LOADS; ++q)
+      if (q >= q0 && q < q1)
+        lds_dma16(buf + static_cast<uint32_t>((wave_u + WAVES * q) * 64 * 16), o[q] + kb, q < Cfg::LOADS_A ? rs_a : rs_b);
+  };
+  auto prologue = [&](const Unit& t, const uint32_t (&o)[LOADS]) {
+#pragma unroll
+    for (int p = 0; p < STAGES - 1; ++p) issue_q(o, t.kt0, min(p, t.nkt - 1), p, 0, LOADS);
+  };
+  // the bias of this lane's columns (split 0 only; the accumulators start there),
+  // or, with overlap, zeros, and the tile's bias (wave 0) and row tokens (wave 1, QKV)
+  // copied into the LDS slots of the unit's parity ahead of the unit's first stage
+  // (bytes past the arrays read as zeros)
+  const int32x4_t rs_bias = buffer_rsrc(g.bias, static_cast<uint32_t>(N) * 4);
+  const int32x4_t rs_idx = buffer_rsrc(g.idx, static_cast<uint32_t>(g.n_max) * 4);
+  const uint32_t side_base = ring_base + static_cast<uint32_t>(STAGES * Cfg::CHUNKS * 16);
+  int parity = 0;
+  auto bias_of = [&](const Unit& t, float4 (&bq)[FN][4]) {
+    if (overlap) {
+      if (wave_u == 0)
+        lds_dma16(side_base + static_cast<uint32_t>(parity * 1024), static_cast<uint32_t>(t.n0 + 4 * lane) * 4, rs_bias);
+      if (KIND == fdh::GEMM_QKV && wave_u == 1)
+        lds_dma16(side_base + static_cast<uint32_t>(2048 + parity * 1024), static_cast<uint32_t>(t.m0 + 4 * lane) * 4, rs_idx);
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) bq[j][q] = make_float4(0.f, 0.f, 0.f, 0.f);
+      return;
+    }
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        bq[j][q] = t.split == 0 ? *reinterpret_cast<const float4*>(g.bias + min(t.n0 + wn * TN + 32 * j + 8 * q + 4 * lg, N - 4))
+                                : make_float4(0.f, 0.f, 0.f, 0.f);
+  };
 
-    // this lane's output rows (one per 32-row block) and their token / request,
-    // loaded before the K loop so that the epilogue never waits on them
-    const int row0 = m0 + wm * TM + l32;
-    int rtok[FM], rreq[FM];
-    row_operands<FM, KIND>(g, M, row0, rtok, rreq);
-
+  Unit cur;
+  int u = blockIdx.x;
+  if (!unit_at(u, cur)) return;
+  uint32_t off[LOADS];
+  offsets(cur, off);
+  // this lane's output rows (one per 32-row block) and their token / request,
+  // loaded before the K loop so that the epilogue never waits on them
+  int rtok[FM], rreq[FM];
+  if constexpr (!overlap) row_operands<FM, KIND>(g, M, cur.m0 + wm * TM + l32, rtok, rreq);
+  float4 bq[FN][4];
+  bias_of(cur, bq);
+  prologue(cur, off);
+  bool stores_in_flight = false;   // the previous unit's epilogue stores follow this unit's first stage
+  for (;;) {
     f32x16_t acc[FM][FN];
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
       for (int j = 0; j < FN; ++j)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+        for (int q = 0; q < 4; ++q) {
+          acc[i][j][4 * q + 0] = bq[j][q].x;
+          acc[i][j][4 * q + 1] = bq[j][q].y;
+          acc[i][j][4 * q + 2] = bq[j][q].z;
+          acc[i][j][4 * q + 3] = bq[j][q].w;
+        }
 
-#pragma unroll
-    for (int p = 0; p < STAGES - 1; ++p) issue(min(p, nkt - 1), p);
+    const int nkt = cur.nkt, kt0 = cur.kt0;
     for (int it = 0; it < nkt; ++it) {
-      // exactly STAGES - 2 younger stages are in flight: stage `it` has landed for every wave
-      wait_vm_barrier<(STAGES - 2) * LOADS>();
+      // exactly STAGES - 2 younger stages (and, in the first step, the previous
+      // unit's epilogue stores) are in flight: stage `it` has landed for every wave
+      if (kOverlap && it == 0 && stores_in_flight)
+        wait_vm_barrier<(STAGES - 2) * LOADS + kEpiStores>();
+      else
+        wait_vm_barrier<(STAGES - 2) * LOADS>();
       // refill the slot every wave finished reading before this barrier (a repeat at the tail)
       const int kt_next = min(it + STAGES - 1, nkt - 1), st_next = (it + STAGES - 1) % STAGES;
-      if constexpr (!Cfg::SPREAD) issue(kt_next, st_next);
+      if constexpr (!Cfg::SPREAD) issue_q(off, kt0, kt_next, st_next, 0, LOADS);
       const uint4* sm = ring_mem + (it % STAGES) * Cfg::CHUNKS;
       bf16x8_t a[2][FM], b[2][FN];
       auto frag = [&](int ks, int slot) {
@@ -385,7 +463,7 @@ FD_DEVICE void gemm_tiles(const fdh::GemmArgs& g, int slots, int M, uint4* ring_
         if (ks + 1 < BK / 16) frag(ks + 1, (ks + 1) & 1);
         if constexpr (Cfg::SPREAD) {
           constexpr int LQ = (LOADS + BK / 16 - 1) / (BK / 16);
-          issue_q(kt_next, st_next, ks * LQ, (ks + 1) * LQ);
+          issue_q(off, kt0, kt_next, st_next, ks * LQ, (ks + 1) * LQ);
         }
 #pragma unroll
         for (int i = 0; i < FM; ++i)
@@ -411,10 +489,14 @@ FD_DEVICE void gemm_tiles(const fdh::GemmArgs& g, int slots, int M, uint4* ring_
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
 
+    const int row0 = cur.m0 + wm * TM + l32, cw = cur.n0 + wn * TN;
+    Unit nxt;
+    u += gridDim.x;
+    const bool more = unit_at(u, nxt);
     if (S > 1) {
       // Store this split's fp32 tile for splitk_reduce_kernel (float4 r4 of block
       // (i, j) of thread t at float4 index ((i * FN + j) * 4 + r4) * THREADS + t).
-      f32x4_t* slot = reinterpret_cast<f32x4_t*>(g.partial + static_cast<size_t>(v) * (BM * BN)) + tid;
+      f32x4_t* slot = reinterpret_cast<f32x4_t*>(g.partial + static_cast<size_t>(cur.v) * (BM * BN)) + tid;
 #pragma unroll
       for (int i = 0; i < FM; ++i)
 #pragma unroll
@@ -423,10 +505,40 @@ FD_DEVICE void gemm_tiles(const fdh::GemmArgs& g, int slots, int M, uint4* ring_
           for (int r4 = 0; r4 < 4; ++r4)
             slot[((i * FN + j) * 4 + r4) * THREADS] =
                 f32x4_t{acc[i][j][4 * r4], acc[i][j][4 * r4 + 1], acc[i][j][4 * r4 + 2], acc[i][j][4 * r4 + 3]};
+    } else if constexpr (overlap) {
+      // the next unit's copies go first; then every epilogue store issues
+      const float* side = reinterpret_cast<const float*>(ring_mem + STAGES * Cfg::CHUNKS);
+      const float* bias_lds = side + parity * 256 + wn * TN;
+      const int* tok_lds = reinterpret_cast<const int*>(side + 512 + parity * 256) + wm * TM + l32;
+      int tok[FM];
+#pragma unroll
+      for (int i = 0; i < FM; ++i) tok[i] = KIND == fdh::GEMM_QKV ? tok_lds[32 * i] : 0;
+      if (more) {
+        parity ^= 1;
+        offsets(nxt, off);
+        bias_of(nxt, bq);
+        prologue(nxt, off);
+      }
+      float4* spare = reinterpret_cast<float4*>(g.partial) + tid;
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          epilogue_block<KIND, true>(g, row0 + 32 * i < M, row0 + 32 * i, cw + 32 * j, lg, tok[i], acc[i][j], spare,
+                                     bias_lds + 32 * j);
+      if (!more) return;
+      stores_in_flight = true;
+      cur = nxt;
       continue;
+    } else {
+      tile_epilogue<FM, FN, KIND>(g, M, row0, cw, lg, rtok, rreq, acc);
     }
-
-    tile_epilogue<FM, FN, KIND>(g, M, row0, n0 + wn * TN, lg, rtok, rreq, acc);
+    if (!more) return;
+    cur = nxt;
+    offsets(cur, off);
+    if constexpr (!overlap) row_operands<FM, KIND>(g, M, cur.m0 + wm * TM + l32, rtok, rreq);
+    bias_of(cur, bq);
+    prologue(cur, off);
   }
 }
 
@@ -463,7 +575,7 @@ __global__ __launch_bounds__(256, 2) void gemm_small_kernel(fdh::GemmArgs g, int
 
 template <int KIND>
 __global__ __launch_bounds__(CfgLarge::THREADS, CfgLarge::OCC) void gemm_large_kernel(fdh::GemmArgs g, int slots) {
-  __shared__ uint4 ring_mem[CfgLarge::STAGES * CfgLarge::CHUNKS];
+  __shared__ uint4 ring_mem[CfgLarge::STAGES * CfgLarge::CHUNKS + kSideChunks];   // ring + bias and token slots
   const int M = min(*g.m, g.n_max);
   if (M <= 0) return;
   gemm_tiles<CfgLarge, KIND>(g, slots, M, ring_mem);
@@ -693,7 +805,11 @@ hipError_t launch_tiled(GemmKind kind, const GemmArgs& a, int max_units, bool la
 hipError_t launch_gemm(GemmKind kind, const GemmArgs& a, hipStream_t s) {
   if (a.K % TBK == 0) {
     const int max_units = a.partial ? a.max_units : 0;   // no scratch: never split
-    if (a.n_max >= kLargeTileRows && a.N >= 1024) return launch_tiled(kind, a, 0, true, s);
+    if (a.n_max >= kLargeTileRows && a.N >= 1024) {
+      // the bf16-output kinds send the stores of rows past M to a spare slot in the scratch
+      if ((kind == GEMM_QKV || kind == GEMM_GELU) && !a.partial) return hipErrorInvalidValue;
+      return launch_tiled(kind, a, 0, true, s);
+    }
     return launch_tiled(kind, a, max_units, false, s);
   }
   const long long tiles = static_cast<long long>((a.n_max + BM - 1) / BM) * ((a.N + BN - 1) / BN);
