@@ -28,7 +28,6 @@ struct BlockWs {
   uint16_t* o;
   uint16_t* g;
   float* partial;      // split-K partial tiles
-  int32_t* counters;   // arrival counters of cut attention items (zeroed at the start of every block)
   float* lse;          // [N][H] base-2 log-sum-exp of each active query's scaled scores
   size_t bytes;
 };
@@ -48,11 +47,9 @@ BlockWs carve_block_ws(const fd_plan* p, const fd_dims* d, void* base) {
   w.q = static_cast<uint16_t*>(take(n * d->D * 2));
   w.o = static_cast<uint16_t*>(take(n * d->D * 2));
   w.g = static_cast<uint16_t*>(take(n * d->F * 2));
-  const size_t tiles = static_cast<size_t>(fdh::gemm_max_tiles());
   const size_t gemm_part = fdh::gemm_scratch_bytes();
   const size_t attn_part = fdh::attn_scratch_bytes(d->dh);
   w.partial = static_cast<float*>(take(gemm_part > attn_part ? gemm_part : attn_part));
-  w.counters = static_cast<int32_t*>(take(tiles * sizeof(int32_t)));
   w.lse = static_cast<float*>(take(n * d->H * sizeof(float)));
   w.bytes = off;
   return w;
@@ -352,7 +349,7 @@ fd_status fd_adaln(const fd_dims* dims, int32_t n_blocks, int32_t n_out, int32_t
   FD_REQUIRE(aligned(w_ada, 16) && aligned(cond, 16), "misaligned buffer");
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   FD_LAUNCH(FD_K_ADALN, s,
-            fdh::launch_adaln(w_ada, b_ada, cond, n_requests, dims->D, n_out, n_blocks, mod, nullptr, 0, s));
+            fdh::launch_adaln(w_ada, b_ada, cond, n_requests, dims->D, n_out, n_blocks, mod, s));
   return FD_OK;
 }
 
@@ -379,14 +376,12 @@ fd_status fd_block_forward(const fd_plan* plan, const fd_dims* dims, const fd_bl
   const int D = dims->D, F = dims->F, B = plan->n_requests, N = plan->n_tokens;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
 
-  // modulation: precomputed by fd_adaln, else computed here (that kernel then also clears the counters)
+  // modulation: precomputed by fd_adaln, else computed here
   const float* mod = w->mod ? w->mod : bw.mod;
   if (!w->mod)
     FD_LAUNCH(FD_K_ADALN, s,
-              fdh::launch_adaln(w->w_ada, w->b_ada, cond, B, D, 6 * D, 1, bw.mod, bw.counters, fdh::gemm_max_tiles(), s));
-  FD_LAUNCH(FD_K_LN, s,
-            fdh::launch_ln_modulate(h, cu_q, B, m, N, D, mod, 6 * D, 0, D, bw.a, w->mod ? bw.counters : nullptr,
-                                    fdh::gemm_max_tiles(), s));
+              fdh::launch_adaln(w->w_ada, w->b_ada, cond, B, D, 6 * D, 1, bw.mod, s));
+  FD_LAUNCH(FD_K_LN, s, fdh::launch_ln_modulate(h, cu_q, B, m, N, D, mod, 6 * D, 0, D, bw.a, s));
   fdh::GemmArgs g{};
   g.n_max = N; g.m = m; g.idx = idx; g.cu_q = cu_q; g.n_req = B; g.D = D;
   g.partial = bw.partial; g.max_units = fdh::gemm_max_tiles();
@@ -395,14 +390,14 @@ fd_status fd_block_forward(const fd_plan* plan, const fd_dims* dims, const fd_bl
   FD_LAUNCH(FD_K_GEMM_QKV, s, fdh::launch_gemm(fdh::GEMM_QKV, g, s));
   FD_LAUNCH(FD_K_ATTN, s,
             fdh::launch_attention(bw.q, k_cache, v_cache, bw.o, D, dims->H, dims->dh, cu_q, plan->req_tok_off, B, N,
-                                  plan->max_request_tokens, bw.partial, bw.counters, bw.lse, s));
+                                  plan->max_request_tokens, bw.partial, bw.lse, s));
   g = fdh::GemmArgs{};
   g.n_max = N; g.m = m; g.idx = idx; g.cu_q = cu_q; g.n_req = B; g.D = D;
   g.partial = bw.partial; g.max_units = fdh::gemm_max_tiles();
   g.act = bw.o; g.wt = w->w_o; g.bias = w->b_o; g.N = D; g.K = D;
   g.out_f32 = h; g.gate = mod + 2 * D; g.gate_stride = 6 * D;
   FD_LAUNCH(FD_K_GEMM_O, s, fdh::launch_gemm(fdh::GEMM_RESID, g, s));
-  FD_LAUNCH(FD_K_LN, s, fdh::launch_ln_modulate(h, cu_q, B, m, N, D, mod, 6 * D, 3 * D, 4 * D, bw.a, nullptr, 0, s));
+  FD_LAUNCH(FD_K_LN, s, fdh::launch_ln_modulate(h, cu_q, B, m, N, D, mod, 6 * D, 3 * D, 4 * D, bw.a, s));
   g = fdh::GemmArgs{};
   g.n_max = N; g.m = m; g.idx = idx; g.cu_q = cu_q; g.n_req = B; g.D = D;
   g.partial = bw.partial; g.max_units = fdh::gemm_max_tiles();
@@ -493,8 +488,8 @@ fd_status fd_final(const fd_plan* plan, const fd_dims* dims, const fd_final_weig
   const int D = dims->D, B = plan->n_requests, N = plan->n_tokens;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   FD_LAUNCH(FD_K_ADALN, s,
-            fdh::launch_adaln(w->w_ada, w->b_ada, cond, B, D, 2 * D, 1, bw.mod, bw.counters, fdh::gemm_max_tiles(), s));
-  FD_LAUNCH(FD_K_LN, s, fdh::launch_ln_modulate(h, cu_q, B, m, N, D, bw.mod, 2 * D, 0, D, bw.a, nullptr, 0, s));
+            fdh::launch_adaln(w->w_ada, w->b_ada, cond, B, D, 2 * D, 1, bw.mod, s));
+  FD_LAUNCH(FD_K_LN, s, fdh::launch_ln_modulate(h, cu_q, B, m, N, D, bw.mod, 2 * D, 0, D, bw.a, s));
   fdh::GemmArgs g{};
   g.n_max = N; g.m = m; g.cu_q = cu_q; g.n_req = B;
   g.partial = bw.partial; g.max_units = fdh::gemm_max_tiles();

@@ -104,10 +104,10 @@ hipError_t launch_scatter_update(const fd_plan* p, int C, float* x, const float*
                                  const int32_t* m, const float* dt, float* vcache, const uint8_t* active,
                                  int skip_mode, hipStream_t s);
 hipError_t launch_adaln(const uint16_t* w, const float* b, const float* cond, int B, int D, int n_out, int n_blocks,
-                        float* mod, int32_t* zero_ints, int n_zero, hipStream_t s);
+                        float* mod, hipStream_t s);
 hipError_t launch_ln_modulate(const float* h, const int32_t* cu_q, int B, const int32_t* m, int n_max, int D,
                               const float* mod, int mod_stride, int shift_off, int scale_off, uint16_t* a,
-                              int32_t* zero_ints, int n_zero, hipStream_t s);
+                              hipStream_t s);
 
 // GEMM epilogue kinds.
 enum GemmKind { GEMM_QKV = 0, GEMM_RESID = 1, GEMM_GELU = 2, GEMM_EMBED = 3, GEMM_OUT = 4 };
@@ -137,7 +137,7 @@ hipError_t launch_gemm(GemmKind kind, const GemmArgs& a, hipStream_t s);
 
 hipError_t launch_attention(const uint16_t* q, const uint16_t* kc, const uint16_t* vc, uint16_t* o, int D, int H,
                             int dh, const int32_t* cu_q, const int32_t* req_tok_off, int B, int n_max,
-                            int max_req_tokens, float* partial, int32_t* counters, float* lse, hipStream_t s);
+                            int max_req_tokens, float* partial, float* lse, hipStream_t s);
 // Region importance (pos: active row of every token, part: [R][H] partial sums).
 size_t importance_lds_bytes(int dh, int max_region_tokens);
 hipError_t launch_importance(const fd_plan* p, int D, int H, int dh, const int32_t* idx, const int32_t* m,

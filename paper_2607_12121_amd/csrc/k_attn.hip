@@ -28,11 +28,11 @@
 // Schedule: the key tiles of all (head, query tile) items, head-major, form one
 // range cut into equal contiguous shares, one per workgroup of the persistent grid;
 // a share that ends inside an item leaves a piece of it to the next share.  Each
-// piece of a cut item stores its unnormalised O, max and sum with device-coherent
-// stores and the last piece to arrive combines them in key order (deterministic
-// for a given grid).  Shares are dealt to the 8 XCDs in contiguous chunks so that
-// the query tiles sharing a head's K/V run on the same L2.  Without scratch for a
-// partial per piece the shares are runs of whole items.
+// piece of a cut item stores its unnormalised O, max and sum, and a second kernel
+// merges the pieces in key order (deterministic for a given grid); no workgroup
+// waits for another.  Shares are dealt to the 8 XCDs in contiguous chunks so that
+// the query tiles sharing a head's K/V run on the same L2.  Head dim 128 and
+// launches without scratch for a partial per piece use runs of whole items.
 #include <type_traits>
 
 #include "fd_common.h"
@@ -116,7 +116,6 @@ struct ACfg {
   static constexpr int OCC = 8 / WAVES;                 // workgroups per CU
   static constexpr int WPE = WAVES * OCC / 4;           // waves per SIMD
   static_assert(THREADS <= kMaxThreads, "partial slots sized for kMaxThreads");
-  static constexpr bool CUT = true;                     // pieces of cut items combined in-kernel
   static_assert(STAGE % (64 * WAVES) == 0, "stage must split into whole wave-loads");
   // split rings: the first half of a wave's loads fetch K blocks, the second half V blocks
   static_assert(!SPLIT || (LOADS % 2 == 0 && TILE / 64 == WAVES * LOADS / 2), "K/V halves of the wave-loads");
@@ -144,32 +143,110 @@ FD_DEVICE bf16x8_t lds_read16(uint32_t addr) {
   return __builtin_bit_cast(bf16x8_t, *(__attribute__((address_space(3))) const u32x4_t*)(uintptr_t)addr);
 }
 
+// Schedule: the key tiles of every item, items head-major, form one range of
+// `work` tile-steps cut into G contiguous shares, one per workgroup, numbered so
+// that each XCD gets consecutive shares (the query tiles of a head share its K/V
+// in that XCD's L2).  With cuts the shares are equal: a share covers the end of
+// one item, whole items and the start of another, and an item covered by
+// several shares is a cut item whose pieces attn_combine_kernel merges.  A share
+// w holds at most two pieces of cut items: the continuation of an item begun in
+// an earlier share (scratch slot 2w) and the first piece of an item that goes on
+// into later shares (slot 2w + 1; when that item starts at the share's start
+// there is no continuation and slot 2w stays unused).  Without cuts every share
+// boundary is rounded up to the next item start.
+struct AttnSched {
+  const int32_t* cu_q;
+  const int32_t* req_tok_off;
+  int B, QB, G;
+  int tiles;              // query tiles over all requests
+  long long work_head;    // tile-steps of one head (key tiles summed over every query tile)
+  long long work;         // ... of every head
+  bool cut;
+
+  FD_DEVICE AttnSched(const int32_t* cq, const int32_t* rto, int B_, int H, int QB_, int G_, int max_units)
+      : cu_q(cq), req_tok_off(rto), B(B_), QB(QB_), G(G_), tiles(0), work_head(0) {
+    for (int b = 0; b < B; ++b) {
+      const int nt = (cu_q[b + 1] - cu_q[b] + QB - 1) / QB;
+      tiles += nt;
+      work_head += static_cast<long long>(nt) * ((req_tok_off[b + 1] - req_tok_off[b] + KB - 1) / KB);
+    }
+    work = work_head * H;
+    // Shares may cut items when the scratch holds two partials per share and
+    // every share gets a tile-step; otherwise every share is a run of whole items.
+    cut = max_units >= 2 * G && work >= static_cast<long long>(G) && G % kXcds == 0;
+  }
+  // the share run by workgroup `blk`
+  FD_DEVICE int share(int blk) const { return (G % kXcds == 0) ? (blk % kXcds) * (G / kXcds) + blk / kXcds : blk; }
+  // tile-step q < work: its item's first tile-step and key tiles, head, request,
+  // the request's first query tile and the query tile
+  FD_DEVICE void locate(long long q, long long& i_start, int& nkv, int& head, int& b, int& first, int& tau) const {
+    head = static_cast<int>(q / work_head);
+    long long r = q - static_cast<long long>(head) * work_head;
+    b = 0;
+    first = 0;
+    nkv = 1;
+    for (; b < B; ++b) {
+      const int nt = (cu_q[b + 1] - cu_q[b] + QB - 1) / QB;
+      nkv = (req_tok_off[b + 1] - req_tok_off[b] + KB - 1) / KB;
+      const long long span = static_cast<long long>(nt) * nkv;
+      if (r < span) break;
+      r -= span;
+      first += nt;
+    }
+    tau = first + static_cast<int>(r / nkv);
+    i_start = q - r % nkv;
+  }
+  FD_DEVICE long long bound(long long x) const {   // first tile-step of share x (x <= G)
+    const long long q = x * work / G;
+    if (cut || q >= work) return q;
+    long long i_start;
+    int nkv, head, b, first, tau;
+    locate(q, i_start, nkv, head, b, first, tau);
+    return i_start == q ? q : i_start + nkv;
+  }
+  FD_DEVICE int share_of(long long q) const {   // the share holding tile-step q
+    int x = static_cast<int>(q * G / work);
+    while (x + 1 < G && bound(x + 1) <= q) ++x;
+    return x;
+  }
+  // scratch slot of piece j of a cut item whose first piece is in share f
+  FD_DEVICE static int slot_of(int f, int j) { return j == 0 ? 2 * f + 1 : 2 * (f + j); }
+};
+
+// Normalised O^T block rows of one 32-query group to bf16 O (row qrow, head
+// columns col0 ...) and the query's base-2 log-sum-exp of the scaled scores
+// (softmax = exp2(s * scale_log2 - lse)); lane (l32, lg) holds query l32 and, in
+// register 4 r4 + e of block dt, d = 32 dt + 8 r4 + 4 lg + e.
+template <int DH>
+FD_DEVICE void store_o(uint16_t* __restrict__ O, float* __restrict__ lse, int D, int H, int head, int qrow, int lg,
+                       const f32x16_t (&oacc)[ACfg<DH>::DT], float m, float l) {
+  if (lse && lg == 0) lse[static_cast<size_t>(qrow) * H + head] = m + __log2f(l);
+  const float inv_l = 1.0f / l;
+  uint16_t* orow = O + static_cast<size_t>(qrow) * D + static_cast<size_t>(head) * DH;
+#pragma unroll
+  for (int dt = 0; dt < ACfg<DH>::DT; ++dt)
+#pragma unroll
+    for (int r4 = 0; r4 < 4; ++r4) {
+      const int d0 = dt * 32 + 8 * r4 + 4 * lg;
+      if (d0 >= DH) continue;
+      uint2 o;
+      o.x = fd::pack_bf2(oacc[dt][4 * r4 + 0] * inv_l, oacc[dt][4 * r4 + 1] * inv_l);
+      o.y = fd::pack_bf2(oacc[dt][4 * r4 + 2] * inv_l, oacc[dt][4 * r4 + 3] * inv_l);
+      *reinterpret_cast<uint2*>(orow + d0) = o;
+    }
+}
+
 template <int DH>
 __global__ __launch_bounds__(ACfg<DH>::THREADS) __attribute__((amdgpu_waves_per_eu(ACfg<DH>::WPE, ACfg<DH>::WPE))) void attn_fwd_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ Kc, const uint16_t* __restrict__ Vc,
     uint16_t* __restrict__ O, int D, int H, const int32_t* __restrict__ cu_q, const int32_t* __restrict__ req_tok_off,
-    int B, float scale_log2, float* __restrict__ partial, int32_t* __restrict__ counters, int max_units,
-    float* __restrict__ lse) {
+    int B, float scale_log2, float* __restrict__ partial, int max_units, float* __restrict__ lse) {
   using C = ACfg<DH>;
   constexpr int DT = C::DT, KS = C::KS, KCH = C::KCH, STAGES = C::STAGES, LOADS = C::LOADS, QG = C::QG, QB = C::QB;
   __shared__ uint4 ring[STAGES][C::STAGE];
-  __shared__ int s_last;
 
-  // query tiles over all requests
-  int tiles = 0;
-  for (int b = 0; b < B; ++b) tiles += (cu_q[b + 1] - cu_q[b] + QB - 1) / QB;
-  if (tiles == 0) return;
-  // tile-steps of one head (key tiles summed over every query tile) and in total
-  long long work_head = 0;
-  for (int b = 0; b < B; ++b)
-    work_head += static_cast<long long>((cu_q[b + 1] - cu_q[b] + QB - 1) / QB) *
-                 ((req_tok_off[b + 1] - req_tok_off[b] + KB - 1) / KB);
-  const long long work = work_head * H;
-  const int G = gridDim.x;
-  // Shares may cut items (partials combined by the last piece to finish) when the
-  // scratch holds two partials per share and every share gets a tile-step;
-  // otherwise every share is a run of whole items.
-  const bool cut = max_units >= 2 * G && work >= static_cast<long long>(G) && G % kXcds == 0;
+  const AttnSched sch(cu_q, req_tok_off, B, H, QB, static_cast<int>(gridDim.x), max_units);
+  if (sch.tiles == 0) return;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l32 = lane & 31, lg = lane >> 5;
@@ -199,11 +276,9 @@ __global__ __launch_bounds__(ACfg<DH>::THREADS) __attribute__((amdgpu_waves_per_
   // One piece of work: key tiles [kt0, kt1) of query tile tau (of request b, whose
   // first query tile is number `first`) under head `head`; piece `piece` of the
   // `npieces` that cover this (head, tile) item in key order, the first of them in
-  // share `share0`, whose arrival counter is that share's.
+  // share `share0`.
   auto run_piece = [&](const int head, const int tau, const int b, const int first, const int kt0, const int kt1,
                        const int piece, const int npieces, const int share0) {
-    // scratch slot of piece j: 2 share0 + 1 for the first, then 2 x (its share)
-    auto slot_of = [&](int j) { return j == 0 ? 2 * share0 + 1 : 2 * (share0 + j); };
     const int q_lo = cu_q[b] + (tau - first) * QB;
     const int q_hi = cu_q[b + 1];
     const int k_beg = req_tok_off[b], k_end = req_tok_off[b + 1];
@@ -586,157 +661,108 @@ __global__ __launch_bounds__(ACfg<DH>::THREADS) __attribute__((amdgpu_waves_per_
 #pragma unroll
     for (int g = 0; g < QG; ++g) l_run[g] = half_sum(l_run[g]);
 
-    if (C::CUT && npieces > 1) {
-      // store this piece's unnormalised O, max and sum (lane-major), count the arrival
+    if (npieces > 1) {
+      // a piece of a cut item: its unnormalised O and (max, sum) for
+      // attn_combine_kernel, lane-major (quad q of thread t at float4 q * THREADS + t,
+      // then the (max, sum) pair of group g at float2 g * THREADS + t)
       constexpr int E = QG * (DT * 16 + 2);
-      float* slot = partial + static_cast<size_t>(slot_of(piece)) * (E * C::THREADS) + tid;
+      float* slot = partial + static_cast<size_t>(AttnSched::slot_of(share0, piece)) * (E * C::THREADS);
+      f32x4_t* quads = reinterpret_cast<f32x4_t*>(slot) + tid;
+      fd::f32x2_t* ml = reinterpret_cast<fd::f32x2_t*>(slot + QG * DT * 16 * C::THREADS) + tid;
 #pragma unroll
       for (int g = 0; g < QG; ++g) {
 #pragma unroll
         for (int d = 0; d < DT; ++d)
 #pragma unroll
-          for (int r = 0; r < 16; ++r)
-            __hip_atomic_store(slot + ((g * DT + d) * 16 + r) * C::THREADS, oacc[g][d][r], __ATOMIC_RELAXED,
-                               __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(slot + (QG * DT * 16 + 2 * g) * C::THREADS, m_run[g], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_store(slot + (QG * DT * 16 + 2 * g + 1) * C::THREADS, l_run[g], __ATOMIC_RELAXED,
-                           __HIP_MEMORY_SCOPE_AGENT);
+          for (int r4 = 0; r4 < 4; ++r4)
+            quads[((g * DT + d) * 4 + r4) * C::THREADS] =
+                f32x4_t{oacc[g][d][4 * r4], oacc[g][d][4 * r4 + 1], oacc[g][d][4 * r4 + 2], oacc[g][d][4 * r4 + 3]};
+        ml[g * C::THREADS] = fd::f32x2_t{m_run[g], l_run[g]};
       }
-      // once the workgroup's stores are done, thread 0 counts the arrival with a release
-      // read-modify-write at agent scope, and the last piece acquires before it reads
-      // the others (the pieces may have run on other XCDs)
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      __syncthreads();
-      if (tid == 0) {
-        const int prev = __hip_atomic_fetch_add(&counters[share0], 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-        if (prev == npieces - 1) {
-          __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
-          __hip_atomic_store(&counters[share0], 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
-        s_last = (prev == npieces - 1);
-      }
-      __syncthreads();
-      if (!s_last) return;
-      // combine the pieces in key order
-      auto piece_base = [&](int j) { return partial + static_cast<size_t>(slot_of(j)) * (E * C::THREADS) + tid; };
-#pragma unroll
-      for (int g = 0; g < QG; ++g) {
-        const int mo = (QG * DT * 16 + 2 * g) * C::THREADS;
-        float m_all = -INFINITY;
-        for (int s2 = 0; s2 < npieces; ++s2)
-          m_all = fmaxf(m_all, __hip_atomic_load(piece_base(s2) + mo, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT));
-        float l_all = 0.f;
-#pragma unroll
-        for (int d = 0; d < DT; ++d)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) oacc[g][d][r] = 0.f;
-        for (int s2 = 0; s2 < npieces; ++s2) {
-          const float* ps = piece_base(s2);
-          // every load of the piece in flight before the first use (the
-          // scheduler would otherwise trade them for registers, one latency each)
-          float pv[DT * 16];
-#pragma unroll
-          for (int e = 0; e < DT * 16; ++e)
-            pv[e] = __hip_atomic_load(ps + (g * DT * 16 + e) * C::THREADS, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          const float ms = __hip_atomic_load(ps + mo, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          const float ls = __hip_atomic_load(ps + mo + C::THREADS, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-          __builtin_amdgcn_sched_barrier(0);
-          const float w = (ms == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(ms - m_all);
-          l_all += w * ls;
-#pragma unroll
-          for (int d = 0; d < DT; ++d)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) oacc[g][d][r] += w * pv[d * 16 + r];
-        }
-        l_run[g] = l_all;
-        m_run[g] = m_all;
-      }
+      return;
     }
-
 #pragma unroll
     for (int g = 0; g < QG; ++g) {
       const int qrow = q_lo + wave * (32 * QG) + g * 32 + l32;
-      if (qrow >= q_hi) continue;
-      // base-2 log-sum-exp of the scaled scores: softmax = exp2(s * scale_log2 - lse)
-      if (lse && lg == 0) lse[static_cast<size_t>(qrow) * H + head] = m_run[g] + __log2f(l_run[g]);
-      const float inv_l = 1.0f / l_run[g];
-      uint16_t* orow = O + static_cast<size_t>(qrow) * D + col0;
-#pragma unroll
-      for (int dt = 0; dt < DT; ++dt)
-#pragma unroll
-        for (int r4 = 0; r4 < 4; ++r4) {
-          const int d0 = dt * 32 + 8 * r4 + 4 * lg;
-          if (d0 >= DH) continue;
-          uint2 o;
-          o.x = fd::pack_bf2(oacc[g][dt][4 * r4 + 0] * inv_l, oacc[g][dt][4 * r4 + 1] * inv_l);
-          o.y = fd::pack_bf2(oacc[g][dt][4 * r4 + 2] * inv_l, oacc[g][dt][4 * r4 + 3] * inv_l);
-          *reinterpret_cast<uint2*>(orow + d0) = o;
-        }
+      if (qrow < q_hi) store_o<DH>(O, lse, D, H, head, qrow, lg, oacc[g], m_run[g], l_run[g]);
     }
   };
 
-  // Schedule: the key tiles of every item, items head-major, form one range of
-  // `work` tile-steps cut into G contiguous shares, one per workgroup, numbered so
-  // that each XCD gets consecutive shares (the query tiles of a head share its K/V
-  // in that XCD's L2).  With cuts the shares are equal: a share covers the end of
-  // one item, whole items and the start of another, and an item covered by
-  // several shares is combined by the last of them to finish.  A share w holds
-  // at most two pieces of cut items: the continuation of an item begun in an
-  // earlier share (scratch slot 2w) and the first piece of an item that goes on
-  // into later shares (slot 2w + 1; when that item starts at the share's start
-  // there is no continuation and slot 2w stays unused).  The arrival counter of a
-  // cut item is its first share's.  Without cuts every share boundary is rounded
-  // up to the next item start.
-  const int w = (G % kXcds == 0) ? (blockIdx.x % kXcds) * (G / kXcds) + blockIdx.x / kXcds : static_cast<int>(blockIdx.x);
-  // tile-step q < work: its item's first tile-step and key tiles, head, request,
-  // the request's first query tile and the query tile
-  auto locate = [&](long long q, long long& i_start, int& nkv, int& head, int& b, int& first, int& tau) {
-    head = static_cast<int>(q / work_head);
-    long long r = q - static_cast<long long>(head) * work_head;
-    b = 0;
-    first = 0;
-    nkv = 1;
-    for (; b < B; ++b) {
-      const int nt = (cu_q[b + 1] - cu_q[b] + QB - 1) / QB;
-      nkv = (req_tok_off[b + 1] - req_tok_off[b] + KB - 1) / KB;
-      const long long span = static_cast<long long>(nt) * nkv;
-      if (r < span) break;
-      r -= span;
-      first += nt;
-    }
-    tau = first + static_cast<int>(r / nkv);
-    i_start = q - r % nkv;
-  };
-  auto bound = [&](long long x) -> long long {   // first tile-step of share x (x <= G)
-    const long long q = x * work / G;
-    if (cut || q >= work) return q;
-    long long i_start;
-    int nkv, head, b, first, tau;
-    locate(q, i_start, nkv, head, b, first, tau);
-    return i_start == q ? q : i_start + nkv;
-  };
-  auto share_of = [&](long long q) {   // the share holding tile-step q
-    int x = static_cast<int>(q * G / work);
-    while (x + 1 < G && bound(x + 1) <= q) ++x;
-    return x;
-  };
-  long long p = bound(w);
-  const long long p_end = bound(w + 1);
+  const int w = sch.share(static_cast<int>(blockIdx.x));
+  long long p = sch.bound(w);
+  const long long p_end = sch.bound(w + 1);
   while (p < p_end) {
     long long i_start;
     int nkv, head, b, first, tau;
-    locate(p, i_start, nkv, head, b, first, tau);
+    sch.locate(p, i_start, nkv, head, b, first, tau);
     if (b >= B) break;   // unreachable: p < work
     const long long i_end = i_start + nkv;
     const int kt0 = static_cast<int>(p - i_start);
     const int kt1 = static_cast<int>((p_end < i_end ? p_end : i_end) - i_start);
     int f = w, l = w;
-    if (cut) {
-      f = share_of(i_start);
-      l = share_of(i_end - 1);
+    if (sch.cut) {
+      f = sch.share_of(i_start);
+      l = sch.share_of(i_end - 1);
     }
     run_piece(head, tau, b, first, kt0, kt1, w - f, l - f + 1, f);
     p = i_start + kt1;
+  }
+}
+
+// The pieces of the cut items, merged in key order (deterministic for a given
+// grid): workgroup x of the attention's grid takes the cut item whose first piece
+// share x holds, if any, with the attention's thread geometry.  The kernel
+// boundary orders the pieces' stores before these loads.
+template <int DH>
+__global__ __launch_bounds__(ACfg<DH>::THREADS) void attn_combine_kernel(
+    uint16_t* __restrict__ O, int D, int H, const int32_t* __restrict__ cu_q, const int32_t* __restrict__ req_tok_off,
+    int B, const float* __restrict__ partial, int max_units, float* __restrict__ lse) {
+  using C = ACfg<DH>;
+  constexpr int DT = C::DT, QG = C::QG, QB = C::QB, E = QG * (DT * 16 + 2);
+  const AttnSched sch(cu_q, req_tok_off, B, H, QB, static_cast<int>(gridDim.x), max_units);
+  if (sch.tiles == 0 || !sch.cut) return;
+  const int x = sch.share(static_cast<int>(blockIdx.x));
+  const long long p0 = sch.bound(x), p_end = sch.bound(x + 1);
+  if (p_end <= p0) return;
+  // the item of the share's last tile-step: cut with its first piece here iff it
+  // starts in this share and goes on past it
+  long long i_start;
+  int nkv, head, b, first, tau;
+  sch.locate(p_end - 1, i_start, nkv, head, b, first, tau);
+  if (b >= B || i_start < p0 || i_start + nkv <= p_end) return;
+  const int npieces = sch.share_of(i_start + nkv - 1) - x + 1;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l32 = lane & 31, lg = lane >> 5;
+  const int q_lo = cu_q[b] + (tau - first) * QB, q_hi = cu_q[b + 1];
+  auto slot = [&](int j) { return partial + static_cast<size_t>(AttnSched::slot_of(x, j)) * (E * C::THREADS); };
+  auto ml_of = [&](int j, int g) {
+    return reinterpret_cast<const fd::f32x2_t*>(slot(j) + QG * DT * 16 * C::THREADS)[g * C::THREADS + tid];
+  };
+#pragma unroll
+  for (int g = 0; g < QG; ++g) {
+    const int qrow = q_lo + wave * (32 * QG) + g * 32 + l32;
+    float m_all = -INFINITY;
+    for (int j = 0; j < npieces; ++j) m_all = fmaxf(m_all, ml_of(j, g)[0]);
+    float l_all = 0.f;
+    f32x16_t oacc[DT];
+#pragma unroll
+    for (int d = 0; d < DT; ++d)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) oacc[d][r] = 0.f;
+    for (int j = 0; j < npieces; ++j) {
+      const f32x4_t* quads = reinterpret_cast<const f32x4_t*>(slot(j)) + tid;
+      // every load of the piece in flight before the first use
+      f32x4_t pv[DT * 4];
+#pragma unroll
+      for (int q = 0; q < DT * 4; ++q) pv[q] = quads[(g * DT * 4 + q) * C::THREADS];
+      const fd::f32x2_t mls = ml_of(j, g);
+      const float wgt = (mls[0] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mls[0] - m_all);
+      l_all += wgt * mls[1];
+#pragma unroll
+      for (int d = 0; d < DT; ++d)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) oacc[d][r] += wgt * pv[d * 4 + r / 4][r % 4];
+    }
+    if (qrow < q_hi) store_o<DH>(O, lse, D, H, head, qrow, lg, oacc, m_all, l_all);
   }
 }
 
@@ -753,13 +779,13 @@ size_t attn_scratch_bytes(int dh) {
 
 hipError_t launch_attention(const uint16_t* q, const uint16_t* kc, const uint16_t* vc, uint16_t* o, int D, int H,
                             int dh, const int32_t* cu_q, const int32_t* req_tok_off, int B, int n_max,
-                            int max_req_tokens, float* partial, int32_t* counters, float* lse, hipStream_t s) {
+                            int max_req_tokens, float* partial, float* lse, hipStream_t s) {
   const int occ = dh >= 128 ? ACfg<128>::OCC : ACfg<64>::OCC;
   const int slots = occ * num_cus();
-  // head dim 128: every workgroup runs whole (head, query tile) items (the long key
-  // range of each item keeps the rounds balanced), so no piece is handed to another
-  // workgroup; smaller heads cut items into pieces combined by the last one
-  const int max_units = (partial && counters && dh < 128) ? gemm_max_tiles() : 0;
+  // head dim 128: every workgroup runs whole (head, query tile) items (cut items
+  // measured no faster: the kernel runs at the power limit); smaller heads cut items
+  // into pieces that attn_combine_kernel merges
+  const int max_units = (partial && dh < 128) ? gemm_max_tiles() : 0;
   // persistent grid: the resident slots, fewer when even one key tile per share
   // would leave some idle (upper bound on the items: every request adds at most
   // one partial query tile)
@@ -771,8 +797,10 @@ hipError_t launch_attention(const uint16_t* q, const uint16_t* kc, const uint16_
   grid = ((grid + kXcds - 1) / kXcds) * kXcds;
   const float scale_log2 = 1.4426950408889634f / sqrtf(static_cast<float>(dh));
 #define FD_ATTN_LAUNCH(DHV)                                                                                         \
-  attn_fwd_kernel<DHV><<<grid, ACfg<DHV>::THREADS, 0, s>>>(q, kc, vc, o, D, H, cu_q, req_tok_off, B, scale_log2, partial, counters, \
-                                                 max_units, lse)
+  attn_fwd_kernel<DHV><<<grid, ACfg<DHV>::THREADS, 0, s>>>(q, kc, vc, o, D, H, cu_q, req_tok_off, B, scale_log2, partial, \
+                                                           max_units, lse);                                           \
+  if (max_units > 0)                                                                                                  \
+    attn_combine_kernel<DHV><<<grid, ACfg<DHV>::THREADS, 0, s>>>(o, D, H, cu_q, req_tok_off, B, partial, max_units, lse)
   switch (dh) {
     case 16: FD_ATTN_LAUNCH(16); break;
     case 64: FD_ATTN_LAUNCH(64); break;

@@ -79,14 +79,10 @@ template <int NB, int KIT>
 __global__ __launch_bounds__(kAdaThreads) void adaln_stream_kernel(const uint16_t* __restrict__ W,
                                                                    const float* __restrict__ bias,
                                                                    const float* __restrict__ cond, int B, int D,
-                                                                   int n_out, int n_rows, float* __restrict__ mod,
-                                                                   int32_t* __restrict__ zero_ints, int n_zero) {
+                                                                   int n_out, int n_rows, float* __restrict__ mod) {
   constexpr int R = kAdaRows;
   extern __shared__ float sc[];   // [NB][D]
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  // The block's first kernel also clears the GEMM split-K arrival counters.
-  if (blockIdx.x == 0 && zero_ints)
-    for (int i = threadIdx.x; i < n_zero; i += kAdaThreads) zero_ints[i] = 0;
   const int n_groups = (n_rows + R - 1) / R;
   const int stride = gridDim.x * kAdaWaves;
   auto load = [&](int grp, uint4 (&w)[KIT][R]) {
@@ -141,12 +137,9 @@ template <int NB>
 __global__ __launch_bounds__(kAdaThreads) void adaln_gemv_kernel(const uint16_t* __restrict__ W,
                                                                  const float* __restrict__ bias,
                                                                  const float* __restrict__ cond, int B, int D,
-                                                                 int n_out, int n_rows, float* __restrict__ mod,
-                                                                 int32_t* __restrict__ zero_ints, int n_zero) {
+                                                                 int n_out, int n_rows, float* __restrict__ mod) {
   extern __shared__ float sc[];   // [NB][D]
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  if (blockIdx.x == 0 && zero_ints)
-    for (int i = threadIdx.x; i < n_zero; i += kAdaThreads) zero_ints[i] = 0;
   const int row0 = blockIdx.x * kAdaRowsPerBlock + wave * kAdaRowsPerWave;
   const uint16_t* wr[kAdaRowsPerWave];
 #pragma unroll
@@ -177,11 +170,7 @@ __global__ __launch_bounds__(256) void ln_modulate_kernel(const float* __restric
                                                           const int32_t* __restrict__ cu_q, int B,
                                                           const int32_t* __restrict__ m_dev, int D,
                                                           const float* __restrict__ mod, int mod_stride,
-                                                          int shift_off, int scale_off, uint16_t* __restrict__ a,
-                                                          int32_t* __restrict__ zero_ints, int n_zero) {
-  // optionally the block's first kernel: clear the GEMM / attention arrival counters
-  if (blockIdx.x == 0 && zero_ints)
-    for (int i = threadIdx.x; i < n_zero; i += 256) zero_ints[i] = 0;
+                                                          int shift_off, int scale_off, uint16_t* __restrict__ a) {
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= *m_dev) return;
@@ -236,7 +225,7 @@ __global__ __launch_bounds__(256) void ln_modulate_kernel(const float* __restric
 namespace fdh {
 
 hipError_t launch_adaln(const uint16_t* w, const float* b, const float* cond, int B, int D, int n_out, int n_blocks,
-                        float* mod, int32_t* zero_ints, int n_zero, hipStream_t s) {
+                        float* mod, hipStream_t s) {
   const int n_rows = n_out * n_blocks;
   // requests per pass: B rounded up to a power of two, at most 8 and at most what LDS holds
   const int cap = kAdaLdsFloats / D;   // >= 1 (D <= 12288)
@@ -250,7 +239,7 @@ hipError_t launch_adaln(const uint16_t* w, const float* b, const float* cond, in
     if (grid > (groups + kAdaWaves - 1) / kAdaWaves) grid = (groups + kAdaWaves - 1) / kAdaWaves;
 #define FD_ADA(NB, KIT)                                                                                     \
   adaln_stream_kernel<NB, KIT><<<grid, kAdaThreads, (NB) * D * sizeof(float), s>>>(w, b, cond, B, D, n_out, \
-                                                                                 n_rows, mod, zero_ints, n_zero)
+                                                                                 n_rows, mod)
 #define FD_ADA_NB(NB)             \
   switch (kit) {                  \
     case 1: FD_ADA(NB, 1); break; \
@@ -268,7 +257,7 @@ hipError_t launch_adaln(const uint16_t* w, const float* b, const float* cond, in
   } else {
     const int grid = (n_rows + kAdaRowsPerBlock - 1) / kAdaRowsPerBlock;
 #define FD_ADA(NB) \
-  adaln_gemv_kernel<NB><<<grid, kAdaThreads, (NB) * D * sizeof(float), s>>>(w, b, cond, B, D, n_out, n_rows, mod, zero_ints, n_zero)
+  adaln_gemv_kernel<NB><<<grid, kAdaThreads, (NB) * D * sizeof(float), s>>>(w, b, cond, B, D, n_out, n_rows, mod)
     switch (nb) {
       case 1: FD_ADA(1); break;
       case 2: FD_ADA(2); break;
@@ -282,19 +271,18 @@ hipError_t launch_adaln(const uint16_t* w, const float* b, const float* cond, in
 
 hipError_t launch_ln_modulate(const float* h, const int32_t* cu_q, int B, const int32_t* m, int n_max, int D,
                               const float* mod, int mod_stride, int shift_off, int scale_off, uint16_t* a,
-                              int32_t* zero_ints, int n_zero, hipStream_t s) {
+                              hipStream_t s) {
   const int grid = (n_max + 3) / 4;
   switch (D % 256 == 0 ? D / 256 : 0) {
 #define FD_LN_CASE(V)                                                                                   \
   case V:                                                                                               \
-    ln_modulate_kernel<V><<<grid, 256, 0, s>>>(h, cu_q, B, m, D, mod, mod_stride, shift_off, scale_off, a, zero_ints, n_zero); \
+    ln_modulate_kernel<V><<<grid, 256, 0, s>>>(h, cu_q, B, m, D, mod, mod_stride, shift_off, scale_off, a); \
     break;
     FD_LN_CASE(1) FD_LN_CASE(2) FD_LN_CASE(3) FD_LN_CASE(4) FD_LN_CASE(5) FD_LN_CASE(6) FD_LN_CASE(8)
     FD_LN_CASE(12) FD_LN_CASE(16)
 #undef FD_LN_CASE
     default:
-      ln_modulate_kernel<0><<<grid, 256, 0, s>>>(h, cu_q, B, m, D, mod, mod_stride, shift_off, scale_off, a, zero_ints,
-                                                 n_zero);
+      ln_modulate_kernel<0><<<grid, 256, 0, s>>>(h, cu_q, B, m, D, mod, mod_stride, shift_off, scale_off, a);
   }
   return hipGetLastError();
 }

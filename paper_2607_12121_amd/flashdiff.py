@@ -497,9 +497,9 @@ class SparseStep:
         """Records one step on these tensors into a HIP graph (nothing runs during the
         capture); each replay() runs the step on whatever the tensors then hold, with
         the same state buffers as step().  The step makes no host round trip and no
-        allocation, and every counter its kernels rely on is cleared by a kernel of the
-        step itself, so replays are independent of each other.  Keyword arguments are
-        those of step() except `stream`."""
+        allocation, and no kernel keeps state from one launch to the next, so replays
+        are independent of each other.  Keyword arguments are those of step() except
+        `stream`."""
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
             self.step(x, x_prev, eps, dt, cond, **kw)
