@@ -740,27 +740,42 @@ __global__ __launch_bounds__(ACfg<DH>::THREADS) void attn_combine_kernel(
 #pragma unroll
   for (int g = 0; g < QG; ++g) {
     const int qrow = q_lo + wave * (32 * QG) + g * 32 + l32;
+    // the pieces' maxima four at a time, then their O two at a time (in key order),
+    // each batch's loads in flight before their first use
     float m_all = -INFINITY;
-    for (int j = 0; j < npieces; ++j) m_all = fmaxf(m_all, ml_of(j, g)[0]);
+    for (int j0 = 0; j0 < npieces; j0 += 4) {
+      float mj[4];
+#pragma unroll
+      for (int k = 0; k < 4; ++k) mj[k] = j0 + k < npieces ? ml_of(j0 + k, g)[0] : -INFINITY;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) m_all = fmaxf(m_all, mj[k]);
+    }
     float l_all = 0.f;
     f32x16_t oacc[DT];
 #pragma unroll
     for (int d = 0; d < DT; ++d)
 #pragma unroll
       for (int r = 0; r < 16; ++r) oacc[d][r] = 0.f;
-    for (int j = 0; j < npieces; ++j) {
-      const f32x4_t* quads = reinterpret_cast<const f32x4_t*>(slot(j)) + tid;
-      // every load of the piece in flight before the first use
-      f32x4_t pv[DT * 4];
+    for (int j0 = 0; j0 < npieces; j0 += 2) {
+      f32x4_t pv[2][DT * 4];
+      fd::f32x2_t mls[2];
 #pragma unroll
-      for (int q = 0; q < DT * 4; ++q) pv[q] = quads[(g * DT * 4 + q) * C::THREADS];
-      const fd::f32x2_t mls = ml_of(j, g);
-      const float wgt = (mls[0] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mls[0] - m_all);
-      l_all += wgt * mls[1];
+      for (int k = 0; k < 2; ++k) {
+        const bool has = j0 + k < npieces;
+        const f32x4_t* quads = reinterpret_cast<const f32x4_t*>(slot(has ? j0 + k : j0)) + tid;
 #pragma unroll
-      for (int d = 0; d < DT; ++d)
+        for (int q = 0; q < DT * 4; ++q) pv[k][q] = quads[(g * DT * 4 + q) * C::THREADS];
+        mls[k] = has ? ml_of(j0 + k, g) : fd::f32x2_t{-INFINITY, 0.f};
+      }
 #pragma unroll
-        for (int r = 0; r < 16; ++r) oacc[d][r] += wgt * pv[d * 4 + r / 4][r % 4];
+      for (int k = 0; k < 2; ++k) {
+        const float wgt = (mls[k][0] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mls[k][0] - m_all);
+        l_all += wgt * mls[k][1];
+#pragma unroll
+        for (int d = 0; d < DT; ++d)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) oacc[d][r] += wgt * pv[k][d * 4 + r / 4][r % 4];
+      }
     }
     if (qrow < q_hi) store_o<DH>(O, lse, D, H, head, qrow, lg, oacc, m_all, l_all);
   }

@@ -15,7 +15,9 @@ the algorithmic bytes of the launches of one kernel and grid, from which GB/s
 and the fraction of the peak follow.
 
 `traffic` turns two `--pmc` passes (FETCH_SIZE, then WRITE_SIZE; both in KiB per
-dispatch) into HBM bytes per launch of one kernel.  Each counter is scaled by
+dispatch) into HBM bytes per launch of one kernel (with further `--kernel`
+regexes: plus the kernels that follow it in the same launch, such as a merge
+pass).  Each counter is scaled by
 what it reads for a plain copy kernel of S bytes launched in the same run (the
 copy reads S and writes S bytes), so the figure is in the copy's units.  The
 summary records the sha256 of the kernel's sources (code only: comments and
@@ -83,8 +85,11 @@ def _per_dispatch(path: str, counter: str, regex: str):
 
 
 def traffic(a) -> str:
-    fetch = _per_dispatch(a.fetch, "FETCH_SIZE", a.kernel)
-    write = _per_dispatch(a.write, "WRITE_SIZE", a.kernel)
+    # a launch is one dispatch of the first kernel regex and at most one of each
+    # further one (a kernel that follows it in the same launch; none is allowed)
+    kernels = a.kernel
+    fetch = _per_dispatch(a.fetch, "FETCH_SIZE", kernels[0])
+    write = _per_dispatch(a.write, "WRITE_SIZE", kernels[0])
     cf = _per_dispatch(a.fetch, "FETCH_SIZE", a.copy_kernel)
     cw = _per_dispatch(a.write, "WRITE_SIZE", a.copy_kernel)
     if not (fetch and write and cf and cw):
@@ -95,15 +100,25 @@ def traffic(a) -> str:
     w_scale = kib / max(v for v, _ in cw.values())
     f_kib = sum(v for v, _ in fetch.values()) / len(fetch)
     w_kib = sum(v for v, _ in write.values()) / len(write)
+    rows = [f"| dispatches of `{kernels[0]}` (fetch pass / write pass) | {len(fetch)} / {len(write)} |",
+            f"| FETCH_SIZE per dispatch, KiB | {f_kib:,.1f} |",
+            f"| WRITE_SIZE per dispatch, KiB | {w_kib:,.1f} |"]
+    for k in kernels[1:]:
+        f2 = _per_dispatch(a.fetch, "FETCH_SIZE", k)
+        w2 = _per_dispatch(a.write, "WRITE_SIZE", k)
+        f2_kib = sum(v for v, _ in f2.values()) / len(fetch)   # per launch of the first kernel
+        w2_kib = sum(v for v, _ in w2.values()) / len(write)
+        rows += [f"| dispatches of `{k}` (fetch pass / write pass) | {len(f2)} / {len(w2)} |",
+                 f"| its FETCH_SIZE per launch, KiB | {f2_kib:,.1f} |",
+                 f"| its WRITE_SIZE per launch, KiB | {w2_kib:,.1f} |"]
+        f_kib += f2_kib
+        w_kib += w2_kib
     bytes_per_launch = (f_kib * f_scale + w_kib * w_scale) * 1024.0
     out = [f"# {a.title}", "", "commands (run from the repo root on an MI355X):", ""]
     out += [f"    {c}" for c in a.cmd]
-    out += ["", f"kernel regex: `{a.kernel}`; copy kernel regex: `{a.copy_kernel}`, "
+    out += ["", "kernel regex: " + " + ".join(f"`{k}`" for k in kernels) + f"; copy kernel regex: `{a.copy_kernel}`, "
                 f"{a.copy_bytes} bytes read and written per copy launch", "",
-            "| figure | value |", "|---|---|",
-            f"| dispatches (fetch pass / write pass) | {len(fetch)} / {len(write)} |",
-            f"| FETCH_SIZE per dispatch, KiB | {f_kib:,.1f} |",
-            f"| WRITE_SIZE per dispatch, KiB | {w_kib:,.1f} |",
+            "| figure | value |", "|---|---|"] + rows + [
             f"| copy FETCH_SIZE per dispatch, KiB (max of {len(cf)}) | {max(v for v, _ in cf.values()):,.1f} |",
             f"| copy WRITE_SIZE per dispatch, KiB (max of {len(cw)}) | {max(v for v, _ in cw.values()):,.1f} |",
             f"| fetch scale (copy bytes / copy counter) | {f_scale:.4f} |",
@@ -169,7 +184,8 @@ def main(argv=None):
     t = sub.add_parser("traffic")
     t.add_argument("--fetch", required=True)
     t.add_argument("--write", required=True)
-    t.add_argument("--kernel", required=True)
+    t.add_argument("--kernel", required=True, action="append",
+                   help="kernel regex; repeat for kernels that follow it within one launch")
     t.add_argument("--copy-kernel", required=True)
     t.add_argument("--copy-bytes", type=int, required=True)
     t.add_argument("--source", nargs="+", required=True)
