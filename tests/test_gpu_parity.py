@@ -359,6 +359,32 @@ def test_many_requests_varlen(base):
     gh.say(f"  M={g['M']}: " + ", ".join(f"{k}={v:.2e}" for k, v in errs.items()))
 
 
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("active", ["all", "one"])
+def test_large_tile_edges(active):
+    """16384 tokens select the eight-wave 256x256 GEMM tile.  Hidden 384 makes the
+    QKV output 1152 wide (the fifth column tile is half past N) and the MLP
+    up-projection 1536.  Every region active: workgroups run two units of each,
+    the second one's loads issued before the first one's epilogue stores (the LDS
+    bias and token slots alternate).  One 32-token region active: one row tile, all
+    but 32 of its rows stored to the spare slot."""
+    k = 512 if active == "all" else 1
+    w = small_workload("audio", D=384, H=6, dh=64, F=1536, L=1, requests=(wl.RequestShape("seq", (16384,), (32,)),),
+                       activity="count", activity_args=(k,))
+    case = gh.make_case("audio", workload=w)
+    inp = case.inp
+    eps = np.zeros(1) if active == "all" else inp.eps
+    gh.say(f"large-tile edges ({active}): N={w.N} D={w.D} F={w.F}")
+    g, st = gh.run_gpu(case, eps, inp.x_cur, inp.x_prev)
+    assert g["M"] == (w.N if active == "all" else 32)
+    rows = None
+    if active == "all":
+        rows = np.unique(np.concatenate([[0, 255, 256, w.N - 1], np.random.default_rng(7).choice(w.N, 124, replace=False)]))
+    o = gh.run_oracle(case, eps, inp.x_cur, inp.x_prev, sample_rows=rows)
+    errs = gh.compare_step(case, g, o, inp.x_cur, st)
+    gh.say(f"  M={g['M']}: " + ", ".join(f"{k2}={v:.2e}" for k2, v in errs.items()))
+
+
 def test_single_region_and_single_token_regions():
     reqs = (wl.RequestShape("grid2d", (8, 8), (8, 8)), wl.RequestShape("grid2d", (4, 12), (1, 1)))
     w = small_workload("tiny", requests=reqs, activity="frac", activity_args=(0.3, 0.6), L=1)
