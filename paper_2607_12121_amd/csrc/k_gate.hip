@@ -184,10 +184,13 @@ __global__ __launch_bounds__(kSelThreads) void gate_select_kernel(
 // xa[i] = bf16(x[idx[i]]) for i < M.  A workgroup covers kGatherUnroll * 256 consecutive
 // float4 elements of the [M][C/4] grid; pass k of its threads covers 256 of them
 // (whole rows, coalesced), and every thread issues its kGatherUnroll loads (addresses
-// clamped into the grid) before any store, so each wave keeps 4 KB in flight.
+// clamped into the grid) before any store, so each wave keeps 4 KB in flight.  SH >= 0:
+// C = 4 << SH, so the row of a float4 element is a shift, not a division.
+template <int SH>
 __global__ __launch_bounds__(256) void gather_kernel(const float* __restrict__ x, const int32_t* __restrict__ idx,
-                                                     const int32_t* __restrict__ m_dev, int C,
+                                                     const int32_t* __restrict__ m_dev, int C_,
                                                      uint16_t* __restrict__ xa) {
+  const int C = SH >= 0 ? (4 << SH) : C_;
   const int c4 = C >> 2;
   const int total = (*m_dev) * c4;
   const int first = blockIdx.x * (256 * kGatherUnroll);
@@ -232,14 +235,16 @@ FD_DEVICE float4 euler4(float4 x, float h, float4 f) {
 // decomposition as the gather (kUpdateUnroll * 256 elements per workgroup, every
 // load of a thread issued before its stores); both rows are read with streaming
 // loads (measured 61 -> 65% of HBM peak at 256 requests), as are the gather's
-// (66 -> 68%).
+// (66 -> 68%).  SH as for the gather.
+template <int SH>
 __global__ __launch_bounds__(256) void update_active_kernel(float* __restrict__ x, const float* __restrict__ v,
                                                             const int32_t* __restrict__ idx,
                                                             const int32_t* __restrict__ m_dev,
                                                             const int32_t* __restrict__ token_region,
                                                             const int32_t* __restrict__ region_req,
                                                             const float* __restrict__ dt, int n_req,
-                                                            float* __restrict__ vcache, int C) {
+                                                            float* __restrict__ vcache, int C_) {
+  const int C = SH >= 0 ? (4 << SH) : C_;
   const int c4 = C >> 2;
   const int total = (*m_dev) * c4;
   const int first = blockIdx.x * (256 * kUpdateUnroll);
@@ -340,7 +345,11 @@ hipError_t launch_select(const fd_plan* p, const double* score, const double* ep
 
 hipError_t launch_gather(const fd_plan* p, int C, const float* x, const int32_t* idx, const int32_t* m,
                          uint16_t* xa, hipStream_t s) {
-  gather_kernel<<<unrolled_grid(static_cast<long long>(p->n_tokens) * (C / 4), kGatherUnroll), 256, 0, s>>>(x, idx, m, C, xa);
+  const int grid = unrolled_grid(static_cast<long long>(p->n_tokens) * (C / 4), kGatherUnroll);
+  if (C == 64)   // the paper's workloads: 16 channels x 2 x 2 patches
+    gather_kernel<4><<<grid, 256, 0, s>>>(x, idx, m, C, xa);
+  else
+    gather_kernel<-1><<<grid, 256, 0, s>>>(x, idx, m, C, xa);
   return hipGetLastError();
 }
 
@@ -351,8 +360,12 @@ hipError_t launch_scatter_update(const fd_plan* p, int C, float* x, const float*
   if (skip_mode == FD_SKIP_REUSE_DRIFT)
     update_skipped_kernel<<<stream_grid(el), 256, 0, s>>>(x, vcache, active, p->token_region, p->region_req, dt,
                                                          p->n_tokens, C);
-  update_active_kernel<<<unrolled_grid(el, kUpdateUnroll), 256, 0, s>>>(x, v, idx, m, p->token_region, p->region_req, dt,
-                                                      p->n_requests, vcache, C);
+  if (C == 64)
+    update_active_kernel<4><<<unrolled_grid(el, kUpdateUnroll), 256, 0, s>>>(x, v, idx, m, p->token_region, p->region_req,
+                                                                           dt, p->n_requests, vcache, C);
+  else
+    update_active_kernel<-1><<<unrolled_grid(el, kUpdateUnroll), 256, 0, s>>>(x, v, idx, m, p->token_region, p->region_req,
+                                                                            dt, p->n_requests, vcache, C);
   return hipGetLastError();
 }
 
