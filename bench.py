@@ -42,6 +42,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--workload", default=WORKLOAD, help="video (default), image, audio, packed or tiny")
     ap.add_argument("--cpu-seconds", type=float, default=12.0, help="budget of the CPU oracle sample")
+    ap.add_argument("--cpu-threads", type=int, default=None,
+                    help="cap on the oracle's BLAS threads (default: every host core)")
     ap.add_argument("--no-hbm", action="store_true", help="skip the streaming-kernel bandwidth figures")
     ap.add_argument("--no-secondary", action="store_true", help="skip the secondary image-workload figure")
     ap.add_argument("--no-trajectory", action="store_true", help="skip the chained-trajectory study")
@@ -228,7 +230,7 @@ def traffic_per_launch(kernel: str, workload: str):
     return read_traffic(os.path.join(ROOT, "profiles", f"{kernel}_{workload}_traffic.txt"), srcs)
 
 
-def cpu_baseline(w, params_gpu, M_expected: int, budget_s: float, max_rows: int = 1024):
+def cpu_baseline(w, params_gpu, M_expected: int, budget_s: float, max_rows: int = 1024, threads=None):
     """The oracle on the host cores, on a bounded sample of one step of the same
     workload: the gate and embedding of all rows, then DiT blocks run on a
     sample of at most `max_rows` of the active rows (their keys and values
@@ -236,7 +238,15 @@ def cpu_baseline(w, params_gpu, M_expected: int, budget_s: float, max_rows: int 
     request, their MLP) for as many blocks as fit the budget, then the final
     layer and update of all rows.  Every per-block cost of the oracle is linear
     in the rows it runs, so the step time is extrapolated as the sampled block
-    time x (active rows / sampled rows) x L."""
+    time x (active rows / sampled rows) x L.  threads: cap on the BLAS threads
+    (None: as many as the host gives)."""
+    from threadpoolctl import threadpool_limits
+
+    if threads is not None:
+        with threadpool_limits(limits=threads):
+            r = cpu_baseline(w, params_gpu, M_expected, budget_s, max_rows)
+        r["cores"] = min(r["cores"], threads)
+        return r
     import torch
     from threadpoolctl import threadpool_info
 
@@ -277,7 +287,8 @@ def cpu_baseline(w, params_gpu, M_expected: int, budget_s: float, max_rows: int 
                       orc.FREEZE)
     t_tail = time.perf_counter() - t2
     t_step = t_gate + t_tail + t_blocks / blocks * (M / len(sel)) * w.L
-    threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    # the oracle's parallelism is its BLAS library's thread pool
+    threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] + [1])
     return {"value": M / t_step, "unit": "active tokens/s", "cores": int(threads), "kind": "oracle",
             "sample": f"one {w.name} step (M={M} active rows): gate + embed of all rows, {blocks} of {w.L} DiT "
                       f"blocks on {len(sel)} sampled active rows (scaled by {M / len(sel):.2f} rows and to {w.L} "
@@ -396,7 +407,7 @@ def main():
         out["hbm"] = hbm_streams(torch, fdl, wl)
     if not args.no_cpu_baseline:
         print("[bench] timing the CPU oracle sample", file=sys.stderr, flush=True)
-        out["cpu_baseline"] = cpu_baseline(w, params, M, args.cpu_seconds)
+        out["cpu_baseline"] = cpu_baseline(w, params, M, args.cpu_seconds, threads=args.cpu_threads)
     print(json.dumps(out), flush=True)
     return 0
 
