@@ -251,6 +251,10 @@ __global__ __launch_bounds__(ACfg<DH>::THREADS) __attribute__((amdgpu_waves_per_
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int l32 = lane & 31, lg = lane >> 5;
   const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  // waves w and w + WAVES/2 share a SIMD: the second one issues first when both
+  // are ready, so the pair drifts apart instead of contending for the same pipe
+  // at the same time (image -2%, video -1%)
+  if (wave_u >= C::WAVES / 2) __builtin_amdgcn_s_setprio(1);
   const int32x4_t rs_k = buffer_rsrc(Kc);
   const int32x4_t rs_v = buffer_rsrc(Vc);
   const uint32_t ring_base = static_cast<uint32_t>(reinterpret_cast<uintptr_t>((lds_ptr_t)&ring[0][0]));
