@@ -385,6 +385,25 @@ def test_large_tile_edges(active):
     gh.say(f"  M={g['M']}: " + ", ".join(f"{k2}={v:.2e}" for k2, v in errs.items()))
 
 
+def test_attention_items_cut_into_many_pieces():
+    """One 32-token region active in a 4096-token sequence (audio dims, 16 heads x
+    64): 16 (head, query tile) items of 64 key tiles over a 256-workgroup grid, so
+    each item is cut into 16 pieces and the merge pass walks several batches of
+    maxima and of partial O per query."""
+    w = small_workload("audio", requests=(wl.RequestShape("seq", (4096,), (32,)),), activity="count",
+                       activity_args=(1,), L=1)
+    case = gh.make_case("audio", workload=w)
+    inp = case.inp
+    g, st = gh.run_gpu(case, inp.eps, inp.x_cur, inp.x_prev)
+    assert g["M"] == 32
+    ncu = torch.cuda.get_device_properties(0).multi_processor_count
+    assert _attention_cuts_items(g["cu_q"], case.rmap.req_tok_off, w.H, ncu)
+    gh.say(f"many pieces: M={g['M']} H={w.H} key tiles per item={w.N // 64} CUs={ncu}")
+    o = gh.run_oracle(case, inp.eps, inp.x_cur, inp.x_prev)
+    errs = gh.compare_step(case, g, o, inp.x_cur, st)
+    gh.say("  " + ", ".join(f"{k}={v:.2e}" for k, v in errs.items()))
+
+
 def test_single_region_and_single_token_regions():
     reqs = (wl.RequestShape("grid2d", (8, 8), (8, 8)), wl.RequestShape("grid2d", (4, 12), (1, 1)))
     w = small_workload("tiny", requests=reqs, activity="frac", activity_args=(0.3, 0.6), L=1)
