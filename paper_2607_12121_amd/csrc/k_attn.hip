@@ -28,8 +28,9 @@
 // Schedule: the key tiles of all (head, query tile) items, head-major, form one
 // range cut into equal contiguous shares, one per workgroup of the persistent grid;
 // a share that ends inside an item leaves a piece of it to the next share.  Each
-// piece of a cut item stores its unnormalised O, max and sum, and a second kernel
-// merges the pieces in key order (deterministic for a given grid); no workgroup
+// piece of a cut item stores its O divided by its own sum (bf16), its max and its
+// sum (fp32), and a second kernel merges the pieces in key order, each weighted by
+// 2^(max - overall max) * sum (deterministic for a given grid); no workgroup
 // waits for another.  Shares are dealt to the 8 XCDs in contiguous chunks so that
 // the query tiles sharing a head's K/V run on the same L2.  Head dim 128 and
 // launches without scratch for a partial per piece use runs of whole items.
@@ -666,21 +667,25 @@ __global__ __launch_bounds__(ACfg<DH>::THREADS) __attribute__((amdgpu_waves_per_
     for (int g = 0; g < QG; ++g) l_run[g] = half_sum(l_run[g]);
 
     if (npieces > 1) {
-      // a piece of a cut item: its unnormalised O and (max, sum) for
-      // attn_combine_kernel, lane-major (quad q of thread t at float4 q * THREADS + t,
-      // then the (max, sum) pair of group g at float2 g * THREADS + t)
+      // a piece of a cut item: O / sum rounded to bf16 (a convex combination of V
+      // rows, so bf16 keeps its range) and (max, sum) in fp32 for
+      // attn_combine_kernel, lane-major (the four bf16 of quad q of thread t at
+      // 8-byte word q * THREADS + t, then, past the slot's O area, the (max, sum)
+      // pair of group g at float2 g * THREADS + t)
       constexpr int E = QG * (DT * 16 + 2);
       float* slot = partial + static_cast<size_t>(AttnSched::slot_of(share0, piece)) * (E * C::THREADS);
-      f32x4_t* quads = reinterpret_cast<f32x4_t*>(slot) + tid;
+      uint2* quads = reinterpret_cast<uint2*>(slot) + tid;
       fd::f32x2_t* ml = reinterpret_cast<fd::f32x2_t*>(slot + QG * DT * 16 * C::THREADS) + tid;
 #pragma unroll
       for (int g = 0; g < QG; ++g) {
+        const float inv = l_run[g] > 0.f ? 1.0f / l_run[g] : 0.f;
 #pragma unroll
         for (int d = 0; d < DT; ++d)
 #pragma unroll
           for (int r4 = 0; r4 < 4; ++r4)
             quads[((g * DT + d) * 4 + r4) * C::THREADS] =
-                f32x4_t{oacc[g][d][4 * r4], oacc[g][d][4 * r4 + 1], oacc[g][d][4 * r4 + 2], oacc[g][d][4 * r4 + 3]};
+                make_uint2(fd::pack_bf2(oacc[g][d][4 * r4] * inv, oacc[g][d][4 * r4 + 1] * inv),
+                           fd::pack_bf2(oacc[g][d][4 * r4 + 2] * inv, oacc[g][d][4 * r4 + 3] * inv));
         ml[g * C::THREADS] = fd::f32x2_t{m_run[g], l_run[g]};
       }
       return;
@@ -761,24 +766,30 @@ __global__ __launch_bounds__(ACfg<DH>::THREADS) void attn_combine_kernel(
 #pragma unroll
       for (int r = 0; r < 16; ++r) oacc[d][r] = 0.f;
     for (int j0 = 0; j0 < npieces; j0 += 2) {
-      f32x4_t pv[2][DT * 4];
+      uint2 pv[2][DT * 4];
       fd::f32x2_t mls[2];
 #pragma unroll
       for (int k = 0; k < 2; ++k) {
         const bool has = j0 + k < npieces;
-        const f32x4_t* quads = reinterpret_cast<const f32x4_t*>(slot(has ? j0 + k : j0)) + tid;
+        const uint2* quads = reinterpret_cast<const uint2*>(slot(has ? j0 + k : j0)) + tid;
 #pragma unroll
         for (int q = 0; q < DT * 4; ++q) pv[k][q] = quads[(g * DT * 4 + q) * C::THREADS];
         mls[k] = has ? ml_of(j0 + k, g) : fd::f32x2_t{-INFINITY, 0.f};
       }
 #pragma unroll
       for (int k = 0; k < 2; ++k) {
-        const float wgt = (mls[k][0] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mls[k][0] - m_all);
-        l_all += wgt * mls[k][1];
+        // the piece's O is normalised by its own sum: weight exp2(m_k - m) * l_k
+        const float wl = (mls[k][0] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(mls[k][0] - m_all) * mls[k][1];
+        l_all += wl;
 #pragma unroll
         for (int d = 0; d < DT; ++d)
 #pragma unroll
-          for (int r = 0; r < 16; ++r) oacc[d][r] += wgt * pv[k][d * 4 + r / 4][r % 4];
+          for (int r = 0; r < 16; ++r) {
+            const uint2 w2 = pv[k][d * 4 + r / 4];
+            const uint32_t wd = (r % 4) < 2 ? w2.x : w2.y;
+            const float o = (r % 2) == 0 ? __uint_as_float(wd << 16) : __uint_as_float(wd & 0xffff0000u);
+            oacc[d][r] += wl * o;
+          }
       }
     }
     if (qrow < q_hi) store_o<DH>(O, lse, D, H, head, qrow, lg, oacc, m_all, l_all);

@@ -309,7 +309,7 @@ def _attention_cuts_items(cu_q, req_tok_off, H, num_cus):
     256 for the eight-wave workgroup, key tiles of 64, a grid of at most one
     workgroup per CU, 4 * num_cus partial slots): True when the equal
     per-workgroup shares of the key-tile range may cut (head, query tile) items,
-    whose pieces are then combined by the last one to finish."""
+    whose pieces the merge pass then combines."""
     QB, KB, slots, max_units = 256, 64, num_cus, 4 * num_cus
     act = np.diff(cu_q)
     tok = np.diff(req_tok_off)
