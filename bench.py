@@ -294,7 +294,19 @@ def cpu_baseline(w, params_gpu, M_expected: int, budget_s: float, max_rows: int 
                       f"blocks on {len(sel)} sampled active rows (scaled by {M / len(sel):.2f} rows and to {w.L} "
                       f"blocks), final + update of all rows; {t_gate + t_blocks + t_tail:.1f} s of CPU work; "
                       f"host nproc={os.cpu_count()}",
-            "seconds_per_step": t_step}
+            "seconds_per_step": t_step, "host": {"nproc": os.cpu_count(), "cpu": _cpu_model()}}
+
+
+def _cpu_model() -> str:
+    """The host CPU's model name (first `model name` line of /proc/cpuinfo), or ""."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return ""
 
 
 def trajectory_study(torch, fdl, wl, w, rm, params, kc, vc, plan, d, cond, dt, T: int,
