@@ -259,6 +259,8 @@ fd_status fd_adaln(const fd_dims* dims, int32_t n_blocks, int32_t n_out, int32_t
  *   ws       device scratch of fd_block_ws_size bytes, 256-byte aligned; after
  *            the call it holds this block's queries and per-query softmax
  *            normalisers, which fd_region_importance reads
+ * Errors: FD_E_UNSUPPORTED for plans of more than 1024 requests (the limit of
+ * fd_select as well), FD_E_SHAPE for dims that do not fit or a small workspace.
  */
 size_t fd_block_ws_size(const fd_plan* plan, const fd_dims* dims);
 fd_status fd_block_forward(const fd_plan* plan, const fd_dims* dims, const fd_block_weights* w,

@@ -371,6 +371,10 @@ fd_status fd_block_forward(const fd_plan* plan, const fd_dims* dims, const fd_bl
                  (w->mod ? aligned(w->mod, 16) : aligned(w->w_ada, 16)) && aligned(h, 16) && aligned(k_cache, 16) &&
                  aligned(v_cache, 16) && aligned(ws, kAlign),
              "misaligned buffer");
+  if (plan->n_requests > fdh::kMaxAttnRequests)
+    return fdh::set_error("the block supports at most %d requests per call (%d given)", fdh::kMaxAttnRequests,
+                          plan->n_requests),
+           FD_E_UNSUPPORTED;
   const BlockWs bw = carve_block_ws(plan, dims, ws);
   if (ws_bytes < bw.bytes) return fdh::set_error("block workspace too small (%zu < %zu)", ws_bytes, bw.bytes), FD_E_SHAPE;
   const int D = dims->D, F = dims->F, B = plan->n_requests, N = plan->n_tokens;

@@ -135,6 +135,8 @@ size_t gemm_scratch_bytes();
 int gemm_max_tiles();
 hipError_t launch_gemm(GemmKind kind, const GemmArgs& a, hipStream_t s);
 
+// Requests per attention launch (its schedule tables live in LDS).
+constexpr int kMaxAttnRequests = 1024;
 hipError_t launch_attention(const uint16_t* q, const uint16_t* kc, const uint16_t* vc, uint16_t* o, int D, int H,
                             int dh, const int32_t* cu_q, const int32_t* req_tok_off, int B, int n_max,
                             int max_req_tokens, float* partial, float* lse, hipStream_t s);

@@ -144,6 +144,83 @@ FD_DEVICE bf16x8_t lds_read16(uint32_t addr) {
   return __builtin_bit_cast(bf16x8_t, *(__attribute__((address_space(3))) const u32x4_t*)(uintptr_t)addr);
 }
 
+constexpr int kMaxSchedRequests = fdh::kMaxAttnRequests;
+
+// Per-request prefix tables of the schedule, built once per workgroup: wpre[b] =
+// tile-steps (query tiles x key tiles, one head) of the requests before b, tpre[b]
+// = their query tiles; entry B holds the totals.
+struct SchedTables {
+  long long wpre[kMaxSchedRequests + 1];
+  int tpre[kMaxSchedRequests + 1];
+};
+
+// One exclusive scan over the requests: each thread sums a contiguous run of them,
+// the runs' sums are scanned within each wave (shuffles) and across the waves
+// (LDS), and each thread then writes its run's prefixes.  O(B / threads + log)
+// steps per workgroup instead of a walk over every request.
+template <int THREADS>
+FD_DEVICE void build_sched_tables(SchedTables& t, const int32_t* __restrict__ cu_q,
+                                  const int32_t* __restrict__ req_tok_off, int B, int QB) {
+  constexpr int NW = THREADS / 64;
+  __shared__ long long s_w[NW];
+  __shared__ int s_t[NW];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int per = (B + THREADS - 1) / THREADS;
+  const int b0 = min(tid * per, B), b1 = min(b0 + per, B);
+  auto tiles_of = [&](int b) { return (cu_q[b + 1] - cu_q[b] + QB - 1) / QB; };
+  auto keys_of = [&](int b) { return (req_tok_off[b + 1] - req_tok_off[b] + KB - 1) / KB; };
+  int st = 0;
+  long long sw = 0;
+  for (int b = b0; b < b1; ++b) {
+    const int nt = tiles_of(b);
+    st += nt;
+    sw += static_cast<long long>(nt) * keys_of(b);
+  }
+  int it = st;
+  long long iw = sw;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int yt = __shfl_up(it, o, 64);
+    const long long yw = __shfl_up(iw, o, 64);
+    if (lane >= o) {
+      it += yt;
+      iw += yw;
+    }
+  }
+  if (lane == 63) {
+    s_t[wave] = it;
+    s_w[wave] = iw;
+  }
+  __syncthreads();
+  int pt = it - st;
+  long long pw = iw - sw;
+  for (int w = 0; w < wave; ++w) {
+    pt += s_t[w];
+    pw += s_w[w];
+  }
+  for (int b = b0; b < b1; ++b) {
+    t.tpre[b] = pt;
+    t.wpre[b] = pw;
+    const int nt = tiles_of(b);
+    pt += nt;
+    pw += static_cast<long long>(nt) * keys_of(b);
+  }
+  if (b0 < b1 && b1 == B) {
+    t.tpre[B] = pt;
+    t.wpre[B] = pw;
+  }
+  __syncthreads();
+}
+
+// A wave-uniform value read from LDS, moved to a scalar register so that the loop
+// bounds and branches derived from it stay scalar.
+FD_DEVICE int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+FD_DEVICE long long uniform(long long v) {
+  const uint32_t lo = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(v)));
+  const uint32_t hi = static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<int>(v >> 32)));
+  return static_cast<long long>((static_cast<uint64_t>(hi) << 32) | lo);
+}
+
 // Schedule: the key tiles of every item, items head-major, form one range of
 // `work` tile-steps cut into G contiguous shares, one per workgroup, numbered so
 // that each XCD gets consecutive shares (the query tiles of a head share its K/V
@@ -154,23 +231,18 @@ FD_DEVICE bf16x8_t lds_read16(uint32_t addr) {
 // an earlier share (scratch slot 2w) and the first piece of an item that goes on
 // into later shares (slot 2w + 1; when that item starts at the share's start
 // there is no continuation and slot 2w stays unused).  Without cuts every share
-// boundary is rounded up to the next item start.
+// boundary is rounded up to the next item start.  Requests are found by binary
+// search in the workgroup's prefix tables.
 struct AttnSched {
-  const int32_t* cu_q;
-  const int32_t* req_tok_off;
-  int B, QB, G;
+  const SchedTables* t;
+  int B, G;
   int tiles;              // query tiles over all requests
   long long work_head;    // tile-steps of one head (key tiles summed over every query tile)
   long long work;         // ... of every head
   bool cut;
 
-  FD_DEVICE AttnSched(const int32_t* cq, const int32_t* rto, int B_, int H, int QB_, int G_, int max_units)
-      : cu_q(cq), req_tok_off(rto), B(B_), QB(QB_), G(G_), tiles(0), work_head(0) {
-    for (int b = 0; b < B; ++b) {
-      const int nt = (cu_q[b + 1] - cu_q[b] + QB - 1) / QB;
-      tiles += nt;
-      work_head += static_cast<long long>(nt) * ((req_tok_off[b + 1] - req_tok_off[b] + KB - 1) / KB);
-    }
+  FD_DEVICE AttnSched(const SchedTables* tab, int B_, int H, int G_, int max_units)
+      : t(tab), B(B_), G(G_), tiles(uniform(tab->tpre[B_])), work_head(uniform(tab->wpre[B_])) {
     work = work_head * H;
     // Shares may cut items when the scratch holds two partials per share and
     // every share gets a tile-step; otherwise every share is a run of whole items.
@@ -183,17 +255,19 @@ struct AttnSched {
   FD_DEVICE void locate(long long q, long long& i_start, int& nkv, int& head, int& b, int& first, int& tau) const {
     head = static_cast<int>(q / work_head);
     long long r = q - static_cast<long long>(head) * work_head;
-    b = 0;
-    first = 0;
-    nkv = 1;
-    for (; b < B; ++b) {
-      const int nt = (cu_q[b + 1] - cu_q[b] + QB - 1) / QB;
-      nkv = (req_tok_off[b + 1] - req_tok_off[b] + KB - 1) / KB;
-      const long long span = static_cast<long long>(nt) * nkv;
-      if (r < span) break;
-      r -= span;
-      first += nt;
+    // the request: the largest b < B with wpre[b] <= r, which has tile-steps
+    // (wpre[b + 1] > r); requests without any are passed over
+    int lo = 0, hi = B - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (uniform(t->wpre[mid]) <= r) lo = mid; else hi = mid - 1;
     }
+    b = lo;
+    first = uniform(t->tpre[b]);
+    const int nt = uniform(t->tpre[b + 1]) - first;
+    const long long w0 = uniform(t->wpre[b]);
+    nkv = static_cast<int>((uniform(t->wpre[b + 1]) - w0) / nt);
+    r -= w0;
     tau = first + static_cast<int>(r / nkv);
     i_start = q - r % nkv;
   }
@@ -245,8 +319,10 @@ __global__ __launch_bounds__(ACfg<DH>::THREADS) __attribute__((amdgpu_waves_per_
   using C = ACfg<DH>;
   constexpr int DT = C::DT, KS = C::KS, KCH = C::KCH, STAGES = C::STAGES, LOADS = C::LOADS, QG = C::QG, QB = C::QB;
   __shared__ uint4 ring[STAGES][C::STAGE];
+  __shared__ SchedTables tabs;
 
-  const AttnSched sch(cu_q, req_tok_off, B, H, QB, static_cast<int>(gridDim.x), max_units);
+  build_sched_tables<C::THREADS>(tabs, cu_q, req_tok_off, B, QB);
+  const AttnSched sch(&tabs, B, H, static_cast<int>(gridDim.x), max_units);
   if (sch.tiles == 0) return;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -728,7 +804,9 @@ __global__ __launch_bounds__(ACfg<DH>::THREADS) void attn_combine_kernel(
     int B, const float* __restrict__ partial, int max_units, float* __restrict__ lse) {
   using C = ACfg<DH>;
   constexpr int DT = C::DT, QG = C::QG, QB = C::QB, E = QG * (DT * 16 + 2);
-  const AttnSched sch(cu_q, req_tok_off, B, H, QB, static_cast<int>(gridDim.x), max_units);
+  __shared__ SchedTables tabs;
+  build_sched_tables<C::THREADS>(tabs, cu_q, req_tok_off, B, QB);
+  const AttnSched sch(&tabs, B, H, static_cast<int>(gridDim.x), max_units);
   if (sch.tiles == 0 || !sch.cut) return;
   const int x = sch.share(static_cast<int>(blockIdx.x));
   const long long p0 = sch.bound(x), p_end = sch.bound(x + 1);
@@ -810,6 +888,7 @@ size_t attn_scratch_bytes(int dh) {
 hipError_t launch_attention(const uint16_t* q, const uint16_t* kc, const uint16_t* vc, uint16_t* o, int D, int H,
                             int dh, const int32_t* cu_q, const int32_t* req_tok_off, int B, int n_max,
                             int max_req_tokens, float* partial, float* lse, hipStream_t s) {
+  if (B < 1 || B > kMaxSchedRequests) return hipErrorInvalidValue;   // the schedule tables' size
   const int occ = dh >= 128 ? ACfg<128>::OCC : ACfg<64>::OCC;
   const int slots = occ * num_cus();
   // head dim 128: every workgroup runs whole (head, query tile) items (cut items

@@ -106,6 +106,10 @@ def test_entry_points_validate_before_launch():
     # null weight
     w0 = fdl.FdBlockWeights(*([0x1000] * 9 + [0]))
     assert lib.fd_block_forward(ctypes.byref(plan), ctypes.byref(d), ctypes.byref(w0), *args) == 1
+    # more requests than the attention's schedule tables hold
+    many = fdl.FdPlan(2050, 1025, 1025, 2, 2, *([0x1000] * 6))
+    assert lib.fd_block_forward(ctypes.byref(many), ctypes.byref(d), ctypes.byref(w), *args) == 3
+    assert b"1024 requests" in lib.fd_last_error()
     # select: bad gate parameters, too many regions
     g = fdl.FdGate(-1.0, 0)
     assert lib.fd_select(ctypes.byref(plan), *([0x1000] * 2), g, *([0x1000] * 7), None) == 1
