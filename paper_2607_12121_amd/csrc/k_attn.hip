@@ -145,6 +145,11 @@ FD_DEVICE bf16x8_t lds_read16(uint32_t addr) {
 }
 
 constexpr int kMaxSchedRequests = fdh::kMaxAttnRequests;
+// Up to this many requests the merge pass walks them instead of building the
+// tables (a kernel of its own, without the tables' LDS): most of its workgroups
+// only look up their share and exit, and for a handful of requests the walk
+// costs less than the table build and its barriers.
+constexpr int kWalkRequests = 16;
 
 // Per-request prefix tables of the schedule, built once per workgroup: wpre[b] =
 // tile-steps (query tiles x key tiles, one head) of the requests before b, tpre[b]
@@ -233,16 +238,30 @@ FD_DEVICE long long uniform(long long v) {
 // there is no continuation and slot 2w stays unused).  Without cuts every share
 // boundary is rounded up to the next item start.  Requests are found by binary
 // search in the workgroup's prefix tables.
+template <int QB, bool TABLES>
 struct AttnSched {
-  const SchedTables* t;
+  const SchedTables* t;         // TABLES: the workgroup's prefix tables
+  const int32_t* cu_q;          // else the requests are walked
+  const int32_t* req_tok_off;
   int B, G;
   int tiles;              // query tiles over all requests
   long long work_head;    // tile-steps of one head (key tiles summed over every query tile)
   long long work;         // ... of every head
   bool cut;
 
-  FD_DEVICE AttnSched(const SchedTables* tab, int B_, int H, int G_, int max_units)
-      : t(tab), B(B_), G(G_), tiles(uniform(tab->tpre[B_])), work_head(uniform(tab->wpre[B_])) {
+  FD_DEVICE AttnSched(const SchedTables* tab, const int32_t* cq, const int32_t* rto, int B_, int H, int G_,
+                      int max_units)
+      : t(tab), cu_q(cq), req_tok_off(rto), B(B_), G(G_), tiles(0), work_head(0) {
+    if constexpr (TABLES) {
+      tiles = uniform(t->tpre[B]);
+      work_head = uniform(t->wpre[B]);
+    } else {
+      for (int b = 0; b < B; ++b) {
+        const int nt = (cu_q[b + 1] - cu_q[b] + QB - 1) / QB;
+        tiles += nt;
+        work_head += static_cast<long long>(nt) * ((req_tok_off[b + 1] - req_tok_off[b] + KB - 1) / KB);
+      }
+    }
     work = work_head * H;
     // Shares may cut items when the scratch holds two partials per share and
     // every share gets a tile-step; otherwise every share is a run of whole items.
@@ -255,6 +274,22 @@ struct AttnSched {
   FD_DEVICE void locate(long long q, long long& i_start, int& nkv, int& head, int& b, int& first, int& tau) const {
     head = static_cast<int>(q / work_head);
     long long r = q - static_cast<long long>(head) * work_head;
+    if constexpr (!TABLES) {   // few requests: walk them (requests without tile-steps are passed over)
+      b = 0;
+      first = 0;
+      nkv = 1;
+      for (; b < B; ++b) {
+        const int nt = (cu_q[b + 1] - cu_q[b] + QB - 1) / QB;
+        nkv = (req_tok_off[b + 1] - req_tok_off[b] + KB - 1) / KB;
+        const long long span = static_cast<long long>(nt) * nkv;
+        if (r < span) break;
+        r -= span;
+        first += nt;
+      }
+      tau = first + static_cast<int>(r / nkv);
+      i_start = q - r % nkv;
+      return;
+    }
     // the request: the largest b < B with wpre[b] <= r, which has tile-steps
     // (wpre[b + 1] > r); requests without any are passed over
     int lo = 0, hi = B - 1;
@@ -322,7 +357,7 @@ __global__ __launch_bounds__(ACfg<DH>::THREADS) __attribute__((amdgpu_waves_per_
   __shared__ SchedTables tabs;
 
   build_sched_tables<C::THREADS>(tabs, cu_q, req_tok_off, B, QB);
-  const AttnSched sch(&tabs, B, H, static_cast<int>(gridDim.x), max_units);
+  const AttnSched<QB, true> sch(&tabs, cu_q, req_tok_off, B, H, static_cast<int>(gridDim.x), max_units);
   if (sch.tiles == 0) return;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -749,7 +784,7 @@ __global__ __launch_bounds__(ACfg<DH>::THREADS) __attribute__((amdgpu_waves_per_
       // 8-byte word q * THREADS + t, then, past the slot's O area, the (max, sum)
       // pair of group g at float2 g * THREADS + t)
       constexpr int E = QG * (DT * 16 + 2);
-      float* slot = partial + static_cast<size_t>(AttnSched::slot_of(share0, piece)) * (E * C::THREADS);
+      float* slot = partial + static_cast<size_t>(AttnSched<QB, true>::slot_of(share0, piece)) * (E * C::THREADS);
       uint2* quads = reinterpret_cast<uint2*>(slot) + tid;
       fd::f32x2_t* ml = reinterpret_cast<fd::f32x2_t*>(slot + QG * DT * 16 * C::THREADS) + tid;
 #pragma unroll
@@ -798,15 +833,13 @@ __global__ __launch_bounds__(ACfg<DH>::THREADS) __attribute__((amdgpu_waves_per_
 // grid): workgroup x of the attention's grid takes the cut item whose first piece
 // share x holds, if any, with the attention's thread geometry.  The kernel
 // boundary orders the pieces' stores before these loads.
-template <int DH>
-__global__ __launch_bounds__(ACfg<DH>::THREADS) void attn_combine_kernel(
-    uint16_t* __restrict__ O, int D, int H, const int32_t* __restrict__ cu_q, const int32_t* __restrict__ req_tok_off,
-    int B, const float* __restrict__ partial, int max_units, float* __restrict__ lse) {
+template <int DH, bool TABLES>
+FD_DEVICE void combine_items(uint16_t* __restrict__ O, int D, int H, const int32_t* __restrict__ cu_q,
+                             const int32_t* __restrict__ req_tok_off, int B, const float* __restrict__ partial,
+                             int max_units, float* __restrict__ lse, const SchedTables* tabs) {
   using C = ACfg<DH>;
   constexpr int DT = C::DT, QG = C::QG, QB = C::QB, E = QG * (DT * 16 + 2);
-  __shared__ SchedTables tabs;
-  build_sched_tables<C::THREADS>(tabs, cu_q, req_tok_off, B, QB);
-  const AttnSched sch(&tabs, B, H, static_cast<int>(gridDim.x), max_units);
+  const AttnSched<QB, TABLES> sch(tabs, cu_q, req_tok_off, B, H, static_cast<int>(gridDim.x), max_units);
   if (sch.tiles == 0 || !sch.cut) return;
   const int x = sch.share(static_cast<int>(blockIdx.x));
   const long long p0 = sch.bound(x), p_end = sch.bound(x + 1);
@@ -820,7 +853,7 @@ __global__ __launch_bounds__(ACfg<DH>::THREADS) void attn_combine_kernel(
   const int npieces = sch.share_of(i_start + nkv - 1) - x + 1;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l32 = lane & 31, lg = lane >> 5;
   const int q_lo = cu_q[b] + (tau - first) * QB, q_hi = cu_q[b + 1];
-  auto slot = [&](int j) { return partial + static_cast<size_t>(AttnSched::slot_of(x, j)) * (E * C::THREADS); };
+  auto slot = [&](int j) { return partial + static_cast<size_t>(AttnSched<QB, true>::slot_of(x, j)) * (E * C::THREADS); };
   auto ml_of = [&](int j, int g) {
     return reinterpret_cast<const fd::f32x2_t*>(slot(j) + QG * DT * 16 * C::THREADS)[g * C::THREADS + tid];
   };
@@ -874,6 +907,21 @@ __global__ __launch_bounds__(ACfg<DH>::THREADS) void attn_combine_kernel(
   }
 }
 
+// TABLES: the requests are located in per-workgroup prefix tables (more than
+// kWalkRequests requests), else walked (no LDS, no barrier).
+template <int DH, bool TABLES>
+__global__ __launch_bounds__(ACfg<DH>::THREADS) void attn_combine_kernel(
+    uint16_t* __restrict__ O, int D, int H, const int32_t* __restrict__ cu_q, const int32_t* __restrict__ req_tok_off,
+    int B, const float* __restrict__ partial, int max_units, float* __restrict__ lse) {
+  if constexpr (TABLES) {
+    __shared__ SchedTables tabs;
+    build_sched_tables<ACfg<DH>::THREADS>(tabs, cu_q, req_tok_off, B, ACfg<DH>::QB);
+    combine_items<DH, true>(O, D, H, cu_q, req_tok_off, B, partial, max_units, lse, &tabs);
+  } else {
+    combine_items<DH, false>(O, D, H, cu_q, req_tok_off, B, partial, max_units, lse, nullptr);
+  }
+}
+
 }  // namespace
 
 namespace fdh {
@@ -908,8 +956,12 @@ hipError_t launch_attention(const uint16_t* q, const uint16_t* kc, const uint16_
 #define FD_ATTN_LAUNCH(DHV)                                                                                         \
   attn_fwd_kernel<DHV><<<grid, ACfg<DHV>::THREADS, 0, s>>>(q, kc, vc, o, D, H, cu_q, req_tok_off, B, scale_log2, partial, \
                                                            max_units, lse);                                           \
-  if (max_units > 0)                                                                                                  \
-    attn_combine_kernel<DHV><<<grid, ACfg<DHV>::THREADS, 0, s>>>(o, D, H, cu_q, req_tok_off, B, partial, max_units, lse)
+  if (max_units > 0 && B > kWalkRequests)                                                                             \
+    attn_combine_kernel<DHV, true><<<grid, ACfg<DHV>::THREADS, 0, s>>>(o, D, H, cu_q, req_tok_off, B, partial,          \
+                                                                       max_units, lse);                                 \
+  else if (max_units > 0)                                                                                             \
+    attn_combine_kernel<DHV, false><<<grid, ACfg<DHV>::THREADS, 0, s>>>(o, D, H, cu_q, req_tok_off, B, partial,         \
+                                                                        max_units, lse)
   switch (dh) {
     case 16: FD_ATTN_LAUNCH(16); break;
     case 64: FD_ATTN_LAUNCH(64); break;

@@ -360,6 +360,31 @@ def test_many_requests_varlen(base):
 
 
 @pytest.mark.timeout(600)
+@pytest.mark.parametrize("base,B,dims,max_regions", [("audio", 448, dict(D=256, H=4, dh=64, F=1024), 8),
+                                                     ("tiny", 600, {}, 6)], ids=["dh64-448", "dh16-600"])
+def test_hundreds_of_requests(base, B, dims, max_regions):
+    """Hundreds of requests of 64 to 256 (or 192) tokens through one block: the
+    attention's per-request schedule tables are built by a scan whose request runs
+    span several waves (448 requests over the 512 threads at head dim 64) or hold
+    several requests per thread (600 over the 256 threads at head dim 16), and each
+    piece finds its request by binary search in them."""
+    rng = np.random.default_rng(B)
+    reqs = tuple(wl.RequestShape("seq", (32 * int(n),), (32,)) for n in rng.integers(2, max_regions + 1, size=B))
+    w = small_workload(base, requests=reqs, activity="frac", activity_args=(0.2, 0.7), L=1, **dims)
+    case = gh.make_case(base, workload=w)
+    inp = case.inp
+    gh.say(f"hundreds of requests ({base} dims, head dim {w.dh}): B={w.B} N={w.N} R={w.R}")
+    g, st = gh.run_gpu(case, inp.eps, inp.x_cur, inp.x_prev)
+    assert len(g["cu_q"]) == B + 1 and g["M"] > 0
+    rows = None
+    if base != "tiny":   # the oracle's block on sampled rows (first, last, random)
+        rows = np.unique(np.concatenate([[0, g["M"] - 1], np.random.default_rng(9).choice(g["M"], 254, replace=False)]))
+    o = gh.run_oracle(case, inp.eps, inp.x_cur, inp.x_prev, sample_rows=rows)
+    errs = gh.compare_step(case, g, o, inp.x_cur, st)
+    gh.say(f"  M={g['M']}: " + ", ".join(f"{k}={v:.2e}" for k, v in errs.items()))
+
+
+@pytest.mark.timeout(600)
 @pytest.mark.parametrize("active", ["all", "one"])
 def test_large_tile_edges(active):
     """16384 tokens select the eight-wave 256x256 GEMM tile.  Hidden 384 makes the
