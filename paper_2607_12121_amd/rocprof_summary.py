@@ -14,6 +14,14 @@ launch shape) with the median, minimum and mean duration; a `--bytes` entry give
 the algorithmic bytes of the launches of one kernel and grid, from which GB/s
 and the fraction of the peak follow.
 
+`mfma` turns one `--pmc` pass (SQ_INSTS_MFMA, SQ_VALU_MFMA_BUSY_CYCLES,
+GRBM_GUI_ACTIVE) into MFMA figures per kernel and launch shape (launches of one
+kernel grouped by their MFMA instruction count): the flops the MFMA instructions
+performed, the ratio of the algorithmic flops to them (the rest is tile padding),
+the clock under load (GRBM active cycles of one XCD over the duration), the MFMA
+pipes' busy share of the SIMD cycles at that clock, and the achieved fraction of
+the nominal bf16 peak.
+
 `traffic` turns two `--pmc` passes (FETCH_SIZE, then WRITE_SIZE; both in KiB per
 dispatch) into HBM bytes per launch of one kernel (with further `--kernel`
 regexes: plus the kernels that follow it in the same launch, such as a merge
@@ -161,6 +169,49 @@ def grids(path: str, title: str, cmds, byte_specs, peak_gbs: float, include=None
     return "\n".join(out) + "\n"
 
 
+def mfma(a) -> str:
+    per = defaultdict(lambda: defaultdict(float))
+    meta = {}
+    for r in csv.DictReader(open(a.csv)):
+        k = r["Dispatch_Id"]
+        per[k][r["Counter_Name"]] += float(r["Counter_Value"])
+        meta[k] = (_short(r["Kernel_Name"]), int(r["End_Timestamp"]) - int(r["Start_Timestamp"]))
+    groups = defaultdict(list)
+    for k, c in per.items():
+        name, dur = meta[k]
+        groups[(name, int(c["SQ_INSTS_MFMA"]))].append((dur, c))
+    alg = []
+    for spec in a.alg or ():
+        label, rest = spec.split("@", 1)
+        rx, fl = rest.rsplit("=", 1)
+        alg.append((label, re.compile(rx), float(fl)))
+    out = [f"# {a.title}", "", "commands (run from the repo root on an MI355X):", ""]
+    out += [f"    {c}" for c in a.cmd]
+    out += ["", f"one MFMA instruction = {a.flops_per_mfma} flops (v_mfma_f32_32x32x16_bf16, the only MFMA the kernels "
+                f"issue); {a.simds} SIMDs; GRBM_GUI_ACTIVE summed over {a.xcds} XCDs; nominal peak {a.peak_tflops} TFLOP/s",
+            "", "| kernel | step | launches | avg us | MFMA instructions | MFMA flops | algorithmic / MFMA flops | "
+                "clock GHz | MFMA busy % of SIMD cycles | % of nominal peak |",
+            "|---|---|---|---|---|---|---|---|---|---|"]
+    for (name, n_mfma), L in sorted(groups.items(), key=lambda g: -g[0][1] * len(g[1])):
+        if n_mfma == 0:
+            continue
+        dur_s = sum(d for d, _ in L) / len(L) * 1e-9
+        busy = sum(c["SQ_VALU_MFMA_BUSY_CYCLES"] for _, c in L) / len(L)
+        cyc = sum(c["GRBM_GUI_ACTIVE"] for _, c in L) / len(L) / a.xcds
+        flops = n_mfma * a.flops_per_mfma
+        lab = next(((l, f) for l, rx, f in alg if rx.search(name) and 0.85 <= f / flops <= 1.0001), None)
+        ghz = cyc / dur_s / 1e9
+        ok = ghz <= a.max_clock_ghz
+        out.append(f"| {name[:48]} | {lab[0] if lab else ''} | {len(L)} | {dur_s * 1e6:.1f} | {n_mfma:,} | {flops:.4g} | "
+                   f"{f'{lab[1] / flops:.3f}' if lab else ''} | {f'{ghz:.2f}' if ok else '—'} | "
+                   f"{f'{100 * busy / (a.simds * cyc):.1f}' if ok else '—'} | "
+                   f"{100 * (lab[1] if lab else flops) / dur_s / (a.peak_tflops * 1e12):.1f} |")
+    out += ["", "% of nominal peak uses the algorithmic flops where the step is named, else the MFMA flops.",
+            f"GRBM active cycles include time outside a launch's own timestamps, which overstates the clock of short",
+            f"launches: where it comes out above {a.max_clock_ghz} GHz the clock and the busy share at it are not shown."]
+    return "\n".join(out) + "\n"
+
+
 def read_traffic(path: str, sources):
     """bytes_per_launch from a traffic summary, or None when it is missing or its
     recorded sources differ from `sources` (the kernel changed since the counters)."""
@@ -191,6 +242,16 @@ def main(argv=None):
     t.add_argument("--source", nargs="+", required=True)
     t.add_argument("--title", required=True)
     t.add_argument("--cmd", action="append", required=True)
+    mf = sub.add_parser("mfma")
+    mf.add_argument("csv")
+    mf.add_argument("--title", required=True)
+    mf.add_argument("--cmd", action="append", required=True)
+    mf.add_argument("--alg", action="append", help="LABEL@KERNEL_REGEX=FLOPS: algorithmic flops of one launch")
+    mf.add_argument("--flops-per-mfma", type=int, default=32768)
+    mf.add_argument("--simds", type=int, default=1024)
+    mf.add_argument("--xcds", type=int, default=8)
+    mf.add_argument("--peak-tflops", type=float, default=2500.0)
+    mf.add_argument("--max-clock-ghz", type=float, default=2.4)
     gr = sub.add_parser("grids")
     gr.add_argument("csv")
     gr.add_argument("--title", required=True)
@@ -201,6 +262,8 @@ def main(argv=None):
     a = ap.parse_args(argv)
     if a.what == "stats":
         sys.stdout.write(stats(a.csv, a.title, a.cmd))
+    elif a.what == "mfma":
+        sys.stdout.write(mfma(a))
     elif a.what == "grids":
         sys.stdout.write(grids(a.csv, a.title, a.cmd, a.bytes, a.peak_gbs, a.include))
     else:
