@@ -25,7 +25,7 @@ the nominal bf16 peak.
 `traffic` turns two `--pmc` passes (FETCH_SIZE, then WRITE_SIZE; both in KiB per
 dispatch) into HBM bytes per launch of one kernel (with further `--kernel`
 regexes: plus the kernels that follow it in the same launch, such as a merge
-pass).  Each counter is scaled by
+pass; with --grid, only launches of that size).  Each counter is scaled by
 what it reads for a plain copy kernel of S bytes launched in the same run (the
 copy reads S and writes S bytes), so the figure is in the copy's units.  The
 summary records the sha256 of the kernel's sources (code only: comments and
@@ -79,25 +79,33 @@ def stats(path: str, title: str, cmds) -> str:
     return "\n".join(out) + "\n"
 
 
-def _per_dispatch(path: str, counter: str, regex: str):
-    """{dispatch id: (counter value summed over its dimensions, duration ns)} of matching kernels."""
+def _per_dispatch(path: str, counter: str, regex: str, grid=None):
+    """{dispatch id: (counter value summed over its dimensions, duration ns)} of matching
+    kernels (with `grid`: only launches of that many work-items)."""
     pat = re.compile(regex)
     val = defaultdict(float)
     dur = {}
     for r in csv.DictReader(open(path)):
         if r["Counter_Name"] != counter or not pat.search(r["Kernel_Name"]):
             continue
+        if grid is not None and int(r["Grid_Size"]) != grid:
+            continue
         val[r["Dispatch_Id"]] += float(r["Counter_Value"])
         dur[r["Dispatch_Id"]] = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
     return {k: (val[k], dur[k]) for k in val}
+
+
+def _mean_us(fetch, write) -> float:
+    d = [v for _, v in fetch.values()] + [v for _, v in write.values()]
+    return sum(d) / len(d) / 1e3
 
 
 def traffic(a) -> str:
     # a launch is one dispatch of the first kernel regex and at most one of each
     # further one (a kernel that follows it in the same launch; none is allowed)
     kernels = a.kernel
-    fetch = _per_dispatch(a.fetch, "FETCH_SIZE", kernels[0])
-    write = _per_dispatch(a.write, "WRITE_SIZE", kernels[0])
+    fetch = _per_dispatch(a.fetch, "FETCH_SIZE", kernels[0], a.grid)
+    write = _per_dispatch(a.write, "WRITE_SIZE", kernels[0], a.grid)
     cf = _per_dispatch(a.fetch, "FETCH_SIZE", a.copy_kernel)
     cw = _per_dispatch(a.write, "WRITE_SIZE", a.copy_kernel)
     if not (fetch and write and cf and cw):
@@ -108,7 +116,8 @@ def traffic(a) -> str:
     w_scale = kib / max(v for v, _ in cw.values())
     f_kib = sum(v for v, _ in fetch.values()) / len(fetch)
     w_kib = sum(v for v, _ in write.values()) / len(write)
-    rows = [f"| dispatches of `{kernels[0]}` (fetch pass / write pass) | {len(fetch)} / {len(write)} |",
+    rows = [f"| dispatches of `{kernels[0]}`{f' with {a.grid} work-items' if a.grid else ''} (fetch pass / write pass) "
+            f"| {len(fetch)} / {len(write)} |",
             f"| FETCH_SIZE per dispatch, KiB | {f_kib:,.1f} |",
             f"| WRITE_SIZE per dispatch, KiB | {w_kib:,.1f} |"]
     for k in kernels[1:]:
@@ -133,6 +142,10 @@ def traffic(a) -> str:
             f"| write scale (copy bytes / copy counter) | {w_scale:.4f} |",
             f"| HBM bytes read per launch (scaled) | {f_kib * f_scale * 1024:,.0f} |",
             f"| HBM bytes written per launch (scaled) | {w_kib * w_scale * 1024:,.0f} |", "",
+            *([f"algorithmic bytes per launch: {a.alg_bytes:,.0f} (counted / algorithmic = "
+               f"{bytes_per_launch / a.alg_bytes:.3f}); at the counted launches' mean duration "
+               f"{_mean_us(fetch, write):.1f} us (under counter collection): {a.alg_bytes / _mean_us(fetch, write) / 1e3:,.0f} GB/s algorithmic, "
+               f"{bytes_per_launch / _mean_us(fetch, write) / 1e3:,.0f} GB/s counted", ""] if a.alg_bytes else []),
             f"bytes_per_launch: {bytes_per_launch:.0f}",
             f"source_sha256: {source_digest(a.source)}",
             "sources: " + " ".join(os.path.relpath(p) for p in sorted(a.source))]
@@ -237,6 +250,8 @@ def main(argv=None):
     t.add_argument("--write", required=True)
     t.add_argument("--kernel", required=True, action="append",
                    help="kernel regex; repeat for kernels that follow it within one launch")
+    t.add_argument("--grid", type=int, help="only launches of this many work-items")
+    t.add_argument("--alg-bytes", type=float, help="algorithmic bytes of one launch, for comparison")
     t.add_argument("--copy-kernel", required=True)
     t.add_argument("--copy-bytes", type=int, required=True)
     t.add_argument("--source", nargs="+", required=True)

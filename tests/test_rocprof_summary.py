@@ -51,3 +51,32 @@ def test_traffic_digest_ignores_comments(tmp_path):
     assert rs.source_digest([str(a)]) == d1
     a.write_text("int f() { return 2; }\n")
     assert rs.source_digest([str(a)]) != d1
+
+
+def test_traffic_per_launch_shape(tmp_path):
+    """FETCH/WRITE per dispatch scaled by the copy's readings, only launches of
+    the given grid size, and the counted / algorithmic ratio."""
+    hdr = FIELDS + ["Grid_Size"]
+
+    def write(path, counter, rows):
+        with open(path, "w", newline="") as f:
+            w = csv.DictWriter(f, fieldnames=hdr)
+            w.writeheader()
+            for d, k, v, g in rows:
+                w.writerow(dict(zip(hdr, (d, k, counter, v, 0, 2000, g))))
+    # copy of 1 MiB: FETCH reads 512 KiB (scale 2), WRITE 1024 KiB (scale 1)
+    fetch, wr = tmp_path / "f.csv", tmp_path / "w.csv"
+    write(fetch, "FETCH_SIZE", [("1", "neg_kernel", 512, 1), ("2", "gather_kernel<4>", 100, 64),
+                                ("3", "gather_kernel<4>", 100, 64), ("4", "gather_kernel<4>", 7, 8)])
+    write(wr, "WRITE_SIZE", [("1", "neg_kernel", 1024, 1), ("2", "gather_kernel<4>", 50, 64),
+                             ("3", "gather_kernel<4>", 50, 64), ("4", "gather_kernel<4>", 9, 8)])
+    src = tmp_path / "k.hip"
+    src.write_text("int f();\n")
+    ap = rs.argparse.ArgumentParser()
+    a = ap.parse_args([])
+    a.fetch, a.write, a.kernel, a.copy_kernel, a.copy_bytes = str(fetch), str(wr), ["gather_kernel"], "neg_kernel", 1 << 20
+    a.grid, a.alg_bytes, a.source, a.title, a.cmd = 64, 250 * 1024, [str(src)], "t", ["c"]
+    out = rs.traffic(a)
+    assert "bytes_per_launch: 256000" in out            # (100 * 2 + 50) KiB
+    assert "counted / algorithmic = 1.000" in out
+    assert "with 64 work-items (fetch pass / write pass) | 2 / 2" in out
