@@ -130,7 +130,9 @@ __global__ __launch_bounds__(kAdaThreads) void adaln_stream_kernel(const uint16_
 
 // The same product for any D (and for more than two requests per pass, where the
 // streaming kernel's registers would grow past two waves per SIMD): one group of 4
-// rows per wave, one k-chunk of all 4 rows at a time.
+// rows per wave, one k-chunk of all 4 rows at a time; blockIdx.y picks the batch
+// of NB requests, so the batches of a many-request call run side by side (their
+// re-reads of the same weight rows are served by L2).
 constexpr int kAdaRowsPerWave = 4;
 constexpr int kAdaRowsPerBlock = kAdaRowsPerWave * kAdaWaves;
 template <int NB>
@@ -140,13 +142,15 @@ __global__ __launch_bounds__(kAdaThreads) void adaln_gemv_kernel(const uint16_t*
                                                                  int n_out, int n_rows, float* __restrict__ mod) {
   extern __shared__ float sc[];   // [NB][D]
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int row0 = blockIdx.x * kAdaRowsPerBlock + wave * kAdaRowsPerWave;
-  const uint16_t* wr[kAdaRowsPerWave];
+  const int b0 = blockIdx.y * NB;   // < B by the grid
+  silu_cond_to_lds<NB>(cond, B, D, b0, sc);
+  const int n_groups = (n_rows + kAdaRowsPerBlock - 1) / kAdaRowsPerBlock;
+  for (int grp = blockIdx.x; grp < n_groups; grp += gridDim.x) {   // row groups of this batch
+    const int row0 = grp * kAdaRowsPerBlock + wave * kAdaRowsPerWave;
+    const uint16_t* wr[kAdaRowsPerWave];
 #pragma unroll
-  for (int i = 0; i < kAdaRowsPerWave; ++i)
-    wr[i] = W + static_cast<size_t>(min(row0 + i, n_rows - 1)) * D;   // rows past the end re-read the last
-  for (int b0 = 0; b0 < B; b0 += NB) {
-    silu_cond_to_lds<NB>(cond, B, D, b0, sc);
+    for (int i = 0; i < kAdaRowsPerWave; ++i)
+      wr[i] = W + static_cast<size_t>(min(row0 + i, n_rows - 1)) * D;   // rows past the end re-read the last
     float acc[kAdaRowsPerWave][NB];
 #pragma unroll
     for (int i = 0; i < kAdaRowsPerWave; ++i)
@@ -255,7 +259,14 @@ hipError_t launch_adaln(const uint16_t* w, const float* b, const float* cond, in
 #undef FD_ADA_NB
 #undef FD_ADA
   } else {
-    const int grid = (n_rows + kAdaRowsPerBlock - 1) / kAdaRowsPerBlock;
+    const int batches = (B + nb - 1) / nb;
+    if (batches > 65535) return hipErrorInvalidValue;   // the grid's y extent
+    // about eight workgroups per CU in all; each walks row groups of its batch, so
+    // the batch's SiLU(cond) is computed once per workgroup, not once per row group
+    const int groups = (n_rows + kAdaRowsPerBlock - 1) / kAdaRowsPerBlock;
+    int gx = (8 * num_cus() + batches - 1) / batches;
+    if (gx > groups) gx = groups;
+    const dim3 grid(gx, batches);
 #define FD_ADA(NB) \
   adaln_gemv_kernel<NB><<<grid, kAdaThreads, (NB) * D * sizeof(float), s>>>(w, b, cond, B, D, n_out, n_rows, mod)
     switch (nb) {

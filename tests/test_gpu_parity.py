@@ -522,6 +522,27 @@ def test_block_forward_with_precomputed_modulation_is_identical():
         assert torch.equal(a, b)
 
 
+@pytest.mark.parametrize("D,B,L", [(1536, 1, 2), (1536, 2, 1), (1536, 3, 2), (1024, 8, 1), (1536, 37, 1),
+                                   (256, 448, 2), (1024, 448, 1)])
+def test_adaln_many_requests(D, B, L):
+    """fd_adaln for 1 to 448 requests (the streaming kernel up to two, then the
+    request-batched kernel with a ragged last batch) against the oracle's
+    modulation in fp64."""
+    g = torch.Generator().manual_seed(D + B)
+    w_ada = (0.02 * torch.randn((L, 6 * D, D), generator=g)).to(torch.bfloat16)
+    b_ada = 0.02 * torch.randn((L, 6 * D), generator=g)
+    cond = torch.randn((B, D), generator=g)
+    mod = torch.zeros((L, B, 6 * D), dtype=torch.float32, device="cuda")
+    dims = fdl.dims(64, D, D // 64, 64, 4 * D)
+    fdl.fd_adaln(dims, L, 6 * D, B, w_ada.cuda(), b_ada.cuda(), cond.cuda(), mod)
+    torch.cuda.synchronize()
+    c64 = cond.numpy().astype(np.float64)
+    for l in range(L):
+        ref = np.concatenate(orc.adaln(w_ada[l].to(torch.float64).numpy(), b_ada[l].numpy().astype(np.float64), c64, 6),
+                             axis=-1)
+        assert rel_err(mod[l].cpu().numpy(), ref) < 1e-5, (D, B, l)
+
+
 # ------------------------------------------------------------------ refinement importance
 
 # (workload, blocks, active regions whose importance the oracle computes or None for all)
