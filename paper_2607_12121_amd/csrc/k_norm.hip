@@ -166,6 +166,92 @@ __global__ __launch_bounds__(kAdaThreads) void adaln_gemv_kernel(const uint16_t*
   }
 }
 
+// More than 24 requests: the same product on the matrix cores in fp32
+// (v_mfma_f32_16x16x4f32; the bf16 weights widen exactly, so the precision is
+// that of the fp32 GEMV), 16 requests per workgroup with their SiLU(cond) in LDS
+// (D <= 2048), each wave 32 weight rows (two 16-row blocks), the workgroup
+// walking row tiles of its request batch.  k is permuted so that a lane reads 8
+// consecutive weights of its row: in MFMA step t of a 32-wide k chunk, lane group
+// g (lanes 16g .. 16g + 15) supplies k = 8g + t, to both operands.  Weights are
+// loaded four chunks ahead.  The grid's x extent is a multiple of the 8 XCDs, so
+// all request batches of a row tile run on one XCD and share its weights in L2.
+constexpr int kAdaMfmaReq = 16;
+// Above this many requests the matrix-core kernel beats the GEMV (hidden 1024:
+// 12 requests 68 against 50 us, 24 equal at 74, 32 75 against 80, 64 79 against
+// 115); below it a few request batches leave most of the GPU idle.
+constexpr int kAdaMfmaMinB = 24;
+constexpr int kAdaMfmaMaxD = 2048;
+constexpr int kAdaMfmaWaves = 8;
+constexpr int kAdaMfmaBlk = 2;                                   // 16-row blocks per wave
+constexpr int kAdaMfmaTile = kAdaMfmaWaves * 16 * kAdaMfmaBlk;   // rows per workgroup tile
+constexpr int kAdaMfmaPf = 4;                                    // 32-wide k chunks of weights in flight
+typedef float f32x4v_t __attribute__((ext_vector_type(4)));
+__global__ __launch_bounds__(kAdaMfmaWaves * 64) void adaln_mfma_kernel(const uint16_t* __restrict__ W,
+                                                                       const float* __restrict__ bias,
+                                                                       const float* __restrict__ cond, int B, int D,
+                                                                       int n_out, int n_rows, float* __restrict__ mod) {
+  __shared__ float sc[kAdaMfmaReq * kAdaMfmaMaxD];   // SiLU(cond) [16][D]
+  const int n_tiles = (n_rows + kAdaMfmaTile - 1) / kAdaMfmaTile;
+  if (static_cast<int>(blockIdx.x) >= n_tiles) return;   // grid padded to whole XCD rounds
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int b0 = blockIdx.y * kAdaMfmaReq;   // < B by the grid
+  for (int e = tid; e < kAdaMfmaReq * D; e += kAdaMfmaWaves * 64) {
+    const float z = b0 + e / D < B ? cond[static_cast<size_t>(b0) * D + e] : 0.f;
+    sc[e] = z / (1.0f + __expf(-z));
+  }
+  __syncthreads();
+  const int i16 = lane & 15, g = lane >> 4;
+  const float* srow = sc + i16 * D + 8 * g;   // request b0 + i16, this lane group's k
+  for (int tile = blockIdx.x; tile < n_tiles; tile += gridDim.x) {
+    const int r0 = tile * kAdaMfmaTile + wave * 16 * kAdaMfmaBlk;
+    const uint16_t* wr[kAdaMfmaBlk];
+    f32x4v_t acc[kAdaMfmaBlk];
+    uint4 wq[kAdaMfmaPf][kAdaMfmaBlk];   // chunks k0 + 32 u, u < kAdaMfmaPf, in flight
+#pragma unroll
+    for (int blk = 0; blk < kAdaMfmaBlk; ++blk) {
+      wr[blk] = W + static_cast<size_t>(min(r0 + 16 * blk + i16, n_rows - 1)) * D + 8 * g;
+      acc[blk] = f32x4v_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int u = 0; u < kAdaMfmaPf; ++u) wq[u][blk] = *reinterpret_cast<const uint4*>(wr[blk] + 32 * u);
+    }
+    for (int k0 = 0; k0 < D; k0 += 32 * kAdaMfmaPf) {   // D is a multiple of 32 kAdaMfmaPf
+#pragma unroll
+      for (int u = 0; u < kAdaMfmaPf; ++u) {
+        const int k = k0 + 32 * u;
+        const float4 s0 = *reinterpret_cast<const float4*>(srow + k);
+        const float4 s1 = *reinterpret_cast<const float4*>(srow + k + 4);
+        const float s8[8] = {s0.x, s0.y, s0.z, s0.w, s1.x, s1.y, s1.z, s1.w};
+        float wf[kAdaMfmaBlk][8];
+#pragma unroll
+        for (int blk = 0; blk < kAdaMfmaBlk; ++blk) bf16x8_to_f32(wq[u][blk], wf[blk]);
+        // refill this slot with the chunk kAdaMfmaPf ahead
+        if (k + 32 * kAdaMfmaPf < D) {
+#pragma unroll
+          for (int blk = 0; blk < kAdaMfmaBlk; ++blk)
+            wq[u][blk] = *reinterpret_cast<const uint4*>(wr[blk] + k + 32 * kAdaMfmaPf);
+        }
+#pragma unroll
+        for (int t = 0; t < 8; ++t)
+#pragma unroll
+          for (int blk = 0; blk < kAdaMfmaBlk; ++blk)
+            acc[blk] = __builtin_amdgcn_mfma_f32_16x16x4f32(wf[blk][t], s8[t], acc[blk], 0, 0, 0);
+      }
+    }
+    // lane (i16, g), register r: weight row 16 blk + 4 g + r of the wave, request b0 + i16
+    const int b = b0 + i16;
+#pragma unroll
+    for (int blk = 0; blk < kAdaMfmaBlk; ++blk)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = r0 + 16 * blk + 4 * g + r;
+        if (row < n_rows && b < B) {
+          const int l = row / n_out, jj = row - l * n_out;
+          mod[(static_cast<size_t>(l) * B + b) * n_out + jj] = acc[blk][r] + bias[row];
+        }
+      }
+  }
+}
+
 // a[i] = bf16(LN(h[i]) * (1 + scale_b) + shift_b) for i < M; one wave per row.
 // VEC: float4 pieces per lane (D = 256 * VEC); VEC = 0 selects the scalar path
 // for D not a multiple of 256 (lanes take every 64th element).
@@ -258,6 +344,16 @@ hipError_t launch_adaln(const uint16_t* w, const float* b, const float* cond, in
     }
 #undef FD_ADA_NB
 #undef FD_ADA
+  } else if (B > kAdaMfmaMinB && D <= kAdaMfmaMaxD && D % (32 * kAdaMfmaPf) == 0) {
+    const int batches = (B + kAdaMfmaReq - 1) / kAdaMfmaReq;
+    if (batches > 65535) return hipErrorInvalidValue;   // the grid's y extent
+    // every row tile its own workgroup column (up to eight per CU in all, then
+    // walked), the x extent a multiple of the 8 XCDs
+    const int tiles = (n_rows + kAdaMfmaTile - 1) / kAdaMfmaTile;
+    int gx = (8 * num_cus() + batches - 1) / batches;
+    if (gx > tiles) gx = tiles;
+    gx = (gx + 7) / 8 * 8;
+    adaln_mfma_kernel<<<dim3(gx, batches), kAdaMfmaWaves * 64, 0, s>>>(w, b, cond, B, D, n_out, n_rows, mod);
   } else {
     const int batches = (B + nb - 1) / nb;
     if (batches > 65535) return hipErrorInvalidValue;   // the grid's y extent

@@ -522,12 +522,13 @@ def test_block_forward_with_precomputed_modulation_is_identical():
         assert torch.equal(a, b)
 
 
-@pytest.mark.parametrize("D,B,L", [(1536, 1, 2), (1536, 2, 1), (1536, 3, 2), (1024, 8, 1), (1536, 37, 1),
-                                   (256, 448, 2), (1024, 448, 1)])
+@pytest.mark.parametrize("D,B,L", [(1536, 1, 2), (1536, 2, 1), (1536, 3, 2), (1024, 8, 1), (1024, 20, 2),
+                                   (1536, 37, 1), (256, 448, 2), (1024, 448, 1), (192, 40, 1)])
 def test_adaln_many_requests(D, B, L):
-    """fd_adaln for 1 to 448 requests (the streaming kernel up to two, then the
-    request-batched kernel with a ragged last batch) against the oracle's
-    modulation in fp64."""
+    """fd_adaln for 1 to 448 requests against the oracle's modulation in fp64:
+    the streaming kernel up to two requests, the GEMV over batches of 8 up to 24
+    (and for a hidden size that is not a multiple of 128), the fp32 matrix-core
+    kernel over batches of 16 above, each with a ragged last batch."""
     g = torch.Generator().manual_seed(D + B)
     w_ada = (0.02 * torch.randn((L, 6 * D, D), generator=g)).to(torch.bfloat16)
     b_ada = 0.02 * torch.randn((L, 6 * D), generator=g)
