@@ -385,7 +385,8 @@ fd_status fd_block_forward(const fd_plan* plan, const fd_dims* dims, const fd_bl
   if (!w->mod)
     FD_LAUNCH(FD_K_ADALN, s,
               fdh::launch_adaln(w->w_ada, w->b_ada, cond, B, D, 6 * D, 1, bw.mod, s));
-  FD_LAUNCH(FD_K_LN, s, fdh::launch_ln_modulate(h, cu_q, B, m, N, D, mod, 6 * D, 0, D, bw.a, s));
+  FD_LAUNCH(FD_K_LN, s, fdh::launch_ln_modulate(h, cu_q, B, m, N, D, mod, 6 * D, 0, D, bw.a, idx, plan->token_region,
+                                                        plan->region_req, s));
   fdh::GemmArgs g{};
   g.n_max = N; g.m = m; g.idx = idx; g.cu_q = cu_q; g.n_req = B; g.D = D;
   g.partial = bw.partial; g.max_units = fdh::gemm_max_tiles();
@@ -401,7 +402,8 @@ fd_status fd_block_forward(const fd_plan* plan, const fd_dims* dims, const fd_bl
   g.act = bw.o; g.wt = w->w_o; g.bias = w->b_o; g.N = D; g.K = D;
   g.out_f32 = h; g.gate = mod + 2 * D; g.gate_stride = 6 * D;
   FD_LAUNCH(FD_K_GEMM_O, s, fdh::launch_gemm(fdh::GEMM_RESID, g, s));
-  FD_LAUNCH(FD_K_LN, s, fdh::launch_ln_modulate(h, cu_q, B, m, N, D, mod, 6 * D, 3 * D, 4 * D, bw.a, s));
+  FD_LAUNCH(FD_K_LN, s, fdh::launch_ln_modulate(h, cu_q, B, m, N, D, mod, 6 * D, 3 * D, 4 * D, bw.a, idx,
+                                                        plan->token_region, plan->region_req, s));
   g = fdh::GemmArgs{};
   g.n_max = N; g.m = m; g.idx = idx; g.cu_q = cu_q; g.n_req = B; g.D = D;
   g.partial = bw.partial; g.max_units = fdh::gemm_max_tiles();
@@ -493,7 +495,7 @@ fd_status fd_final(const fd_plan* plan, const fd_dims* dims, const fd_final_weig
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   FD_LAUNCH(FD_K_ADALN, s,
             fdh::launch_adaln(w->w_ada, w->b_ada, cond, B, D, 2 * D, 1, bw.mod, s));
-  FD_LAUNCH(FD_K_LN, s, fdh::launch_ln_modulate(h, cu_q, B, m, N, D, bw.mod, 2 * D, 0, D, bw.a, s));
+  FD_LAUNCH(FD_K_LN, s, fdh::launch_ln_modulate(h, cu_q, B, m, N, D, bw.mod, 2 * D, 0, D, bw.a, nullptr, nullptr, nullptr, s));
   fdh::GemmArgs g{};
   g.n_max = N; g.m = m; g.cu_q = cu_q; g.n_req = B;
   g.partial = bw.partial; g.max_units = fdh::gemm_max_tiles();

@@ -105,8 +105,11 @@ hipError_t launch_scatter_update(const fd_plan* p, int C, float* x, const float*
                                  int skip_mode, hipStream_t s);
 hipError_t launch_adaln(const uint16_t* w, const float* b, const float* cond, int B, int D, int n_out, int n_blocks,
                         float* mod, hipStream_t s);
+// The row's request: from idx and the plan's token -> region -> request tables
+// when idx is given, else by binary search in cu_q.
 hipError_t launch_ln_modulate(const float* h, const int32_t* cu_q, int B, const int32_t* m, int n_max, int D,
                               const float* mod, int mod_stride, int shift_off, int scale_off, uint16_t* a,
+                              const int32_t* idx, const int32_t* token_region, const int32_t* region_req,
                               hipStream_t s);
 
 // GEMM epilogue kinds.

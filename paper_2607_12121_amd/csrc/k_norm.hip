@@ -260,11 +260,16 @@ __global__ __launch_bounds__(256) void ln_modulate_kernel(const float* __restric
                                                           const int32_t* __restrict__ cu_q, int B,
                                                           const int32_t* __restrict__ m_dev, int D,
                                                           const float* __restrict__ mod, int mod_stride,
-                                                          int shift_off, int scale_off, uint16_t* __restrict__ a) {
+                                                          int shift_off, int scale_off, uint16_t* __restrict__ a,
+                                                          const int32_t* __restrict__ idx,
+                                                          const int32_t* __restrict__ token_region,
+                                                          const int32_t* __restrict__ region_req) {
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (row >= *m_dev) return;
-  const int b = fd::row_request(cu_q, B, row);
+  // the row's request: through its token's region when the index list is given
+  // (two table reads after idx, whatever B), else a binary search over cu_q
+  const int b = B == 1 ? 0 : idx ? region_req[token_region[idx[row]]] : fd::row_request(cu_q, B, row);
   const float* hr = h + static_cast<size_t>(row) * D;
   const float* shift = mod + static_cast<size_t>(b) * mod_stride + shift_off;
   const float* scale = mod + static_cast<size_t>(b) * mod_stride + scale_off;
@@ -378,18 +383,21 @@ hipError_t launch_adaln(const uint16_t* w, const float* b, const float* cond, in
 
 hipError_t launch_ln_modulate(const float* h, const int32_t* cu_q, int B, const int32_t* m, int n_max, int D,
                               const float* mod, int mod_stride, int shift_off, int scale_off, uint16_t* a,
+                              const int32_t* idx, const int32_t* token_region, const int32_t* region_req,
                               hipStream_t s) {
   const int grid = (n_max + 3) / 4;
   switch (D % 256 == 0 ? D / 256 : 0) {
 #define FD_LN_CASE(V)                                                                                   \
   case V:                                                                                               \
-    ln_modulate_kernel<V><<<grid, 256, 0, s>>>(h, cu_q, B, m, D, mod, mod_stride, shift_off, scale_off, a); \
+    ln_modulate_kernel<V><<<grid, 256, 0, s>>>(h, cu_q, B, m, D, mod, mod_stride, shift_off, scale_off, a, idx,   \
+                                            token_region, region_req);                                          \
     break;
     FD_LN_CASE(1) FD_LN_CASE(2) FD_LN_CASE(3) FD_LN_CASE(4) FD_LN_CASE(5) FD_LN_CASE(6) FD_LN_CASE(8)
     FD_LN_CASE(12) FD_LN_CASE(16)
 #undef FD_LN_CASE
     default:
-      ln_modulate_kernel<0><<<grid, 256, 0, s>>>(h, cu_q, B, m, D, mod, mod_stride, shift_off, scale_off, a);
+      ln_modulate_kernel<0><<<grid, 256, 0, s>>>(h, cu_q, B, m, D, mod, mod_stride, shift_off, scale_off, a, idx,
+                                                 token_region, region_req);
   }
   return hipGetLastError();
 }
