@@ -384,6 +384,46 @@ def test_hundreds_of_requests(base, B, dims, max_regions):
     gh.say(f"  M={g['M']}: " + ", ".join(f"{k}={v:.2e}" for k, v in errs.items()))
 
 
+def _random_config(seed: int):
+    """A seeded small configuration: head dim, heads, MLP width, latent channels,
+    1 to 40 requests of 1D or 2D token grids with random region sizes."""
+    rng = np.random.default_rng(1000 + seed)
+    dh = int(rng.choice([16, 64, 128]))
+    H = int(rng.integers(1, 5)) * (4 if dh == 16 else 1)
+    D = H * dh
+    if D % 64:
+        H, D = H * 2, D * 2
+    F = 64 * int(rng.integers(1, 9))
+    C = 16 * int(rng.integers(1, 5))
+    B = int(rng.choice([1, 2, 5, 17, 40]))
+    reqs = []
+    for _ in range(B):
+        if rng.random() < 0.5:
+            r = int(rng.choice([4, 8, 16, 32]))
+            reqs.append(wl.RequestShape("seq", (r * int(rng.integers(1, 9)),), (r,)))
+        else:
+            ry, rx = int(rng.choice([2, 4, 8])), int(rng.choice([2, 4, 8]))
+            reqs.append(wl.RequestShape("grid2d", (ry * int(rng.integers(1, 5)), rx * int(rng.integers(1, 5))), (ry, rx)))
+    return dict(C=C, D=D, H=H, dh=dh, F=F, requests=tuple(reqs))
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("seed", range(8))
+def test_random_configurations(seed):
+    """Seeded random small configurations (head dims 16 / 64 / 128, hidden and MLP
+    widths, channels, 1 to 40 requests of mixed 1D / 2D grids and region sizes,
+    20-70% of each request active) through one block against the oracle."""
+    cfg = _random_config(seed)
+    w = small_workload("tiny", activity="frac", activity_args=(0.2, 0.7), L=1, **cfg)
+    case = gh.make_case("tiny", workload=w)
+    inp = case.inp
+    gh.say(f"random {seed}: C={w.C} D={w.D} H={w.H} dh={w.dh} F={w.F} B={w.B} N={w.N} R={w.R}")
+    g, st = gh.run_gpu(case, inp.eps, inp.x_cur, inp.x_prev)
+    o = gh.run_oracle(case, inp.eps, inp.x_cur, inp.x_prev)
+    errs = gh.compare_step(case, g, o, inp.x_cur, st)
+    gh.say(f"  M={g['M']}: " + ", ".join(f"{k}={v:.2e}" for k, v in errs.items()))
+
+
 @pytest.mark.timeout(600)
 @pytest.mark.parametrize("active", ["all", "one"])
 def test_large_tile_edges(active):
