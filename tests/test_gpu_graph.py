@@ -8,6 +8,7 @@ import torch
 from paper_2607_12121_amd import flashdiff as fdl
 from paper_2607_12121_amd import workloads as wl
 from tests import gpu_harness as gh
+from tests.helpers import small_workload
 
 pytestmark = pytest.mark.gpu
 
@@ -19,10 +20,22 @@ def _need_gpu():
     fdl.lib()
 
 
+def _many_requests_workload():
+    """40 requests of 64 to 512 tokens, hidden 256: the attention's schedule tables
+    and its merge pass with tables, and the matrix-core adaLN."""
+    rng = np.random.default_rng(40)
+    reqs = tuple(wl.RequestShape("seq", (32 * int(n),), (32,)) for n in rng.integers(2, 17, size=40))
+    return small_workload("audio", requests=reqs, activity="frac", activity_args=(0.2, 0.7), L=2, D=256, H=4, dh=64,
+                          F=1024)
+
+
 @pytest.mark.timeout(300)
-@pytest.mark.parametrize("name", ["image", "tiny"])
+@pytest.mark.parametrize("name", ["image", "tiny", "many"])
 def test_graph_replays_match_eager(name):
-    case = gh.make_case(name, L=2 if name == "image" else None)
+    if name == "many":
+        case = gh.make_case("audio", workload=_many_requests_workload())
+    else:
+        case = gh.make_case(name, L=2 if name == "image" else None)
     w = case.w
 
     def state():
